@@ -1,0 +1,196 @@
+/*
+ * kvpattn.h — prefix-shared paged-KV attention for mixed RL rollout sessions, on AMD MI355X (gfx950).
+ *
+ * The operations follow the serving model of "Scheduling Mixed RL Rollouts Beyond Prefix Locality"
+ * (MISA-T, arXiv 2608.11152):
+ *   - KV state is held in fixed-size blocks of a paged pool, and each session retains a growing set of
+ *     blocks (Sec. 2.3 on PagedAttention KV management; Sec. 3.2, the retained blocks k_s(t) of Eq. 2);
+ *   - a prompt fans out into grouped samples that share the prompt prefix (Sec. 3.1, group id g_r), and
+ *     prefix reuse is block-granular (Sec. 4.4: the longest matching prompt-block hash is the reusable
+ *     prefix), so a group shares whole pages;
+ *   - a later agentic turn prefills only its L - H new tokens over the cached history H (Eq. 1).
+ * The attention itself is scaled dot-product softmax attention with grouped-query heads: query head h
+ * reads KV head h / (num_q_heads / num_kv_heads).
+ *
+ * Conventions for every entry point
+ *   - Return value: KVP_OK (0) or a negative kvp_status.  On a negative return nothing has been enqueued
+ *     and no output has been touched; kvp_last_error() then holds a human-readable detail (thread-local).
+ *   - "device" pointers are HIP device allocations owned by the caller; they must stay valid until the
+ *     work enqueued on `stream` has completed.  "host" arrays are read during the call only; the library
+ *     keeps no reference to them after it returns.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Every call is asynchronous on it.
+ *   - Page ids read from device block tables are range-checked on the device.  An id outside
+ *     [0, num_pages) is never dereferenced: the kernels skip that page and record KVP_ERANGE in the
+ *     pool's device error word, which kv_pool_device_error() returns.
+ *   - Only bf16 KV pages and bf16 queries are supported (KVP_BF16); outputs may be bf16 or fp32.
+ *   - page_size is 16 tokens; head_dim is 64 or 128; num_q_heads / num_kv_heads is 1, 2, 4, 8 or 16.
+ *
+ * Pool layout in HBM (one layer):  bf16 [num_pages][num_kv_heads][2][16 * head_dim]
+ *   Each (page, kv head) holds a K block then a V block of 16 * head_dim elements each.  Within them,
+ *   token t (0..15 within the page) and dimension c are stored at
+ *     K block:  ((c / 8) * 16 + t) * 8 + (c % 8)                       chunk-major rows of 8 dims
+ *     V block:  (((c / 16) * 2 + s / 8) * 16 + (c % 16)) * 8 + (s % 8)  with slot s = pi(t)
+ *   where pi(t) swaps bits 2 and 3 of t (an involution: V slots 0..7 hold tokens 0-3 and 8-11, slots
+ *   8..15 hold tokens 4-7 and 12-15).  This order makes every operand load of the attention kernels a
+ *   16-byte, fully used, contiguous access.  kv_pool_layer_ptr() exposes the raw layer for inspection.
+ */
+#ifndef KVPATTN_H
+#define KVPATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct kvp_pool* kvp_pool_t; /* opaque; created by kv_pool_create, owned by the library */
+
+typedef enum kvp_status {
+  KVP_OK = 0,
+  KVP_EINVAL = -1,      /* null pointer, bad count, inconsistent shape or dtype                      */
+  KVP_ERANGE = -2,      /* length beyond the block table (maxp * 16), or page id outside the pool    */
+  KVP_EGROUP = -3,      /* bad group id, shared prefix longer than a member, or members' tables differ */
+  KVP_ESHARED = -4,     /* kv_append would write into a page shared by a rollout group               */
+  KVP_EWORKSPACE = -5,  /* workspace smaller than the size query returned                            */
+  KVP_EUNSUPPORTED = -6,/* head_dim, page size, dtype or GQA ratio not supported                     */
+  KVP_EHIP = -7,        /* HIP runtime error (detail in kvp_last_error)                              */
+  KVP_ENOMEM = -8       /* device or pinned-host allocation failed                                   */
+} kvp_status;
+
+typedef enum kvp_dtype { KVP_BF16 = 0, KVP_F32 = 1 } kvp_dtype;
+
+/* Rollout-group prefix sharing (Sec. 3.1 group id g_r; Sec. 4.4 block-granular reuse).
+ *   group_id[i]      host int32 [num_seqs]: group of sequence i, or -1 if ungrouped.
+ *   shared_pages[g]  host int32 [num_groups]: the first shared_pages[g] entries of every member's block
+ *                    table are the same physical pages (the group's whole prompt pages).
+ * For decode it is an optimisation hint: the shared prefix is read once per group and merged with each
+ * member's private suffix by a log-sum-exp combine; the result equals the ungrouped result. */
+typedef struct kvp_group_prefix {
+  const int32_t* group_id;
+  const int32_t* shared_pages;
+  int32_t num_groups;
+} kvp_group_prefix;
+
+/* ---------------------------------------------------------------------------------------------------
+ * Pool (Sec. 3.2: sessions retain KV blocks of a fixed-capacity instance pool)
+ * ------------------------------------------------------------------------------------------------- */
+
+/* Allocate a zero-filled pool of num_layers x num_pages pages on the current HIP device.
+ * page_size must be 16, head_dim 64 or 128, dtype KVP_BF16.  *out receives the handle. */
+int kv_pool_create(kvp_pool_t* out, int num_layers, int num_pages, int page_size, int num_kv_heads,
+                   int head_dim, int dtype);
+
+/* Free the pool and its device memory (synchronises the device first).  NULL is accepted. */
+int kv_pool_destroy(kvp_pool_t pool);
+
+/* Zero every page and clear the device error word, enqueued on `stream` (the weight-sync cache reset
+ * of Sec. 5.2: cached prefixes become invalid after new weights are loaded). */
+int kv_pool_reset(kvp_pool_t pool, void* stream);
+
+/* Device address and byte size of one layer of the pool (layout in the file header). */
+int kv_pool_layer_ptr(kvp_pool_t pool, int layer, void** dev_ptr, size_t* bytes);
+
+/* Pool geometry: any output pointer may be NULL. */
+int kv_pool_info(kvp_pool_t pool, int* num_layers, int* num_pages, int* num_kv_heads, int* head_dim);
+
+/* Synchronise the device, then return (in *code) and clear the first device-side error recorded by
+ * kernels using this pool (KVP_OK if none). */
+int kv_pool_device_error(kvp_pool_t pool, int* code);
+
+/* ---------------------------------------------------------------------------------------------------
+ * kv_append — write new tokens' K/V into their paged slots (a session's retained blocks grow, Sec. 3.2)
+ * ------------------------------------------------------------------------------------------------- */
+
+/* Sequence i appends the tokens k[cu_new[i] .. cu_new[i+1]) at logical positions start_pos[i] + j; the
+ * token at position p goes to page block_tables[i * maxp + p / 16], slot p % 16, of every KV head.
+ *   k, v          device bf16 [cu_new[num_seqs], num_kv_heads, head_dim] (token-major)
+ *   block_tables  device int32 [num_seqs, maxp]
+ *   start_pos     host int32 [num_seqs];  cu_new host int32 [num_seqs + 1], non-decreasing, cu_new[0]=0
+ *   gp            host, nullable.  When given, a write into any of a member's first shared_pages[g]
+ *                 pages is refused with KVP_ESHARED (shared prompt pages are written once, before the
+ *                 group is formed, by an append without gp).
+ * Errors: KVP_ERANGE if start_pos[i] + count > maxp * 16.  The copy is bit-exact. */
+int kv_append(kvp_pool_t pool, int layer, const void* k, const void* v, const int32_t* block_tables,
+              int maxp, const int32_t* start_pos, const int32_t* cu_new, int num_seqs,
+              const kvp_group_prefix* gp, void* stream);
+
+/* Read back tokens [0, lens[i]) of every sequence in logical order (inverse of kv_append), for
+ * inspection and tests.  k_out, v_out: device bf16 [sum(lens), num_kv_heads, head_dim];
+ * block_tables device int32 [num_seqs, maxp]; lens host int32 [num_seqs]. */
+int kv_gather(kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp, const int32_t* lens,
+              int num_seqs, void* k_out, void* v_out, void* stream);
+
+/* ---------------------------------------------------------------------------------------------------
+ * paged_decode_attn — one query token per sequence over its paged KV (Sec. 3.1 groups, Sec. 4.4 reuse)
+ * ------------------------------------------------------------------------------------------------- */
+
+/* Workspace bytes paged_decode_attn needs for these lengths / groups (host arrays as below). */
+int paged_decode_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int num_seqs,
+                                const kvp_group_prefix* group_prefix, int num_q_heads, size_t* bytes);
+
+/* out[i, h, :] = softmax(scale * q[i,h,:] . K_i[t, g(h), :]) over t < seq_lens[i], applied to V_i,
+ * where K_i / V_i are read through block_tables row i and g(h) = h / (num_q_heads / num_kv_heads).
+ *   q             device bf16 [num_seqs, num_q_heads, head_dim]
+ *   block_tables  device int32 [num_seqs, maxp]
+ *   seq_lens      host int32 [num_seqs]: cached tokens including the current one (0 = zero output)
+ *   group_prefix  host, nullable: members' shared prompt pages are read once per group
+ *   out           device [num_seqs, num_q_heads, head_dim], out_dtype KVP_BF16 or KVP_F32
+ *   ws            device workspace of ws_bytes >= paged_decode_workspace_size(...)
+ * Errors: KVP_ERANGE if seq_lens[i] > maxp * 16; KVP_EGROUP if a group id is out of range or a member's
+ * seq_len is shorter than its group's shared pages; KVP_EWORKSPACE if ws_bytes is too small. */
+int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
+                      const int32_t* seq_lens, int num_seqs, const kvp_group_prefix* group_prefix,
+                      int num_q_heads, float scale, void* out, int out_dtype, void* ws, size_t ws_bytes,
+                      void* stream);
+
+/* ---------------------------------------------------------------------------------------------------
+ * prefix_chunk_prefill_attn — a new chunk attends to its cached history plus itself (Eq. 1: only the
+ * L - H uncached tokens are prefilled over the reusable prefix H)
+ * ------------------------------------------------------------------------------------------------- */
+
+/* Workspace bytes prefix_chunk_prefill_attn needs. */
+int prefix_chunk_prefill_workspace_size(kvp_pool_t pool, const int32_t* ctx_lens, const int32_t* cu_q,
+                                        int num_seqs, int num_q_heads, size_t* bytes);
+
+/* Session i's chunk queries q[cu_q[i] + j] sit at positions ctx_lens[i] + j, and row j attends keys
+ * [0, ctx_lens[i] + j] of its sequence (bottom-right causal).  The chunk's own K/V must already have
+ * been appended.
+ *   q             device bf16 [cu_q[num_seqs], num_q_heads, head_dim]
+ *   block_tables  device int32 [num_seqs, maxp] (row i = session i)
+ *   ctx_lens      host int32 [num_seqs];  cu_q host int32 [num_seqs + 1]
+ *   out           device [cu_q[num_seqs], num_q_heads, head_dim], out_dtype KVP_BF16 or KVP_F32
+ * Errors: KVP_ERANGE if ctx_lens[i] + chunk > maxp * 16; KVP_EWORKSPACE if ws_bytes is too small. */
+int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables,
+                              int maxp, const int32_t* ctx_lens, const int32_t* cu_q, int num_seqs,
+                              int num_q_heads, float scale, void* out, int out_dtype, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------------------------
+ * Host-side checks and diagnostics
+ * ------------------------------------------------------------------------------------------------- */
+
+/* Full host validation of a host copy of the block tables: every entry a sequence of length lens[i]
+ * uses is in [0, num_pages) (else KVP_ERANGE), and every group member's first shared_pages[g] entries
+ * equal those of the group's first member (else KVP_EGROUP).  gp may be NULL. */
+int kvp_check_tables(const int32_t* block_tables_host, int maxp, const int32_t* lens, int num_seqs,
+                     int num_pages, const kvp_group_prefix* gp);
+
+/* Decode work plan, for inspection and tests (pure host computation, no device needed).
+ * Writes up to cap items of 8 int32 each into items_out:
+ *   {kind (0 = private, 1 = shared prefix), table row, page_lo, page_hi, token_end, first member,
+ *    member count, partial slot (-1 = writes the final output)}
+ * and returns the item count in *n_items (which may exceed cap), the number of partial slots in
+ * *n_partials, and the chosen pages per split in *pages_per_split. */
+int kvp_plan_decode(const int32_t* seq_lens, int num_seqs, const kvp_group_prefix* gp, int num_q_heads,
+                    int num_kv_heads, int32_t* items_out, int cap, int* n_items, int* n_partials,
+                    int* pages_per_split);
+
+const char* kvp_strerror(int code);
+const char* kvp_last_error(void);
+const char* kvp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KVPATTN_H */

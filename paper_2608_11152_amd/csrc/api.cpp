@@ -1,0 +1,544 @@
+// C-ABI of libkvpattn: pool management, kv_append / kv_gather, paged_decode_attn and
+// prefix_chunk_prefill_attn.  Host metadata is validated and planned here, packed into one buffer and
+// uploaded with a single asynchronous copy from a ring of pinned staging slots; then the kernels are
+// launched on the caller's stream.  Nothing in this file computes attention.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kvp_kernels.h"
+
+struct kvp_pool {
+  int num_layers = 0, num_pages = 0, num_kv_heads = 0, head_dim = 0, device = 0;
+  size_t layer_bytes = 0;
+  unsigned char* base = nullptr;  // [layers][pages][Hkv][2][16*d] bf16
+  int* err = nullptr;             // device error word
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int set_err(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int from_status(const kvp::Status& s) {
+  if (!s.ok()) g_last_error = s.msg;
+  return s.code;
+}
+
+int hip_err(hipError_t e, const char* what) {
+  return set_err(KVP_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Ring of pinned host staging slots.  A slot is reused only after the copy that last read it has
+// completed (its event), so consecutive calls do not wait on each other's GPU work.
+class Staging {
+ public:
+  int upload(void* dst, const void* src, size_t n, hipStream_t s) {
+    if (n == 0) return KVP_OK;
+    std::lock_guard<std::mutex> lock(mu_);
+    Slot& sl = slots_[next_];
+    next_ = (next_ + 1) % kSlots;
+    if (sl.pending) {
+      hipError_t e = hipEventSynchronize(sl.ev);
+      if (e != hipSuccess) return hip_err(e, "hipEventSynchronize(staging)");
+      sl.pending = false;
+    }
+    if (!sl.ev) {
+      hipError_t e = hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming);
+      if (e != hipSuccess) return hip_err(e, "hipEventCreate");
+    }
+    if (n > sl.cap) {
+      if (sl.host) (void)hipHostFree(sl.host);
+      sl.host = nullptr;
+      sl.cap = 0;
+      const size_t cap = std::max<size_t>(n, 1 << 20);
+      hipError_t e = hipHostMalloc(&sl.host, cap, hipHostMallocDefault);
+      if (e != hipSuccess) return set_err(KVP_ENOMEM, "hipHostMalloc(%zu): %s", cap, hipGetErrorString(e));
+      sl.cap = cap;
+    }
+    std::memcpy(sl.host, src, n);
+    hipError_t e = hipMemcpyAsync(dst, sl.host, n, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_err(e, "hipMemcpyAsync(metadata)");
+    e = hipEventRecord(sl.ev, s);
+    if (e != hipSuccess) return hip_err(e, "hipEventRecord");
+    sl.pending = true;
+    return KVP_OK;
+  }
+
+ private:
+  static constexpr int kSlots = 8;
+  struct Slot {
+    void* host = nullptr;
+    size_t cap = 0;
+    hipEvent_t ev = nullptr;
+    bool pending = false;
+  };
+  std::mutex mu_;
+  Slot slots_[kSlots];
+  int next_ = 0;
+};
+
+Staging& staging() {
+  static Staging* s = new Staging();  // intentionally leaked: outlives static destruction order
+  return *s;
+}
+
+// Packs several arrays into one host buffer with 256-byte aligned offsets.
+struct Packer {
+  std::vector<unsigned char> buf;
+  size_t add(const void* p, size_t n) {
+    const size_t off = (buf.size() + 255) & ~size_t(255);
+    buf.resize(off + n);
+    if (n) std::memcpy(buf.data() + off, p, n);
+    return off;
+  }
+  size_t size() const { return (buf.size() + 255) & ~size_t(255); }
+};
+
+bool pool_ok(kvp_pool_t p) { return p && p->base; }
+
+int check_layer(kvp_pool_t pool, int layer) {
+  if (!pool_ok(pool)) return set_err(KVP_EINVAL, "pool is NULL or destroyed");
+  if (layer < 0 || layer >= pool->num_layers)
+    return set_err(KVP_EINVAL, "layer %d outside [0, %d)", layer, pool->num_layers);
+  return KVP_OK;
+}
+
+const uint16_t* layer_ptr(kvp_pool_t pool, int layer) {
+  return reinterpret_cast<const uint16_t*>(pool->base + (size_t)layer * pool->layer_bytes);
+}
+
+// Page runs of a set of token ranges: sequence i covers positions [start[i], start[i] + cnt[i]).
+void build_runs(const int32_t* start, const int64_t* first_src, const int32_t* cnt, int B,
+                std::vector<kvp::PageRun>* runs) {
+  runs->clear();
+  for (int i = 0; i < B; ++i) {
+    if (cnt[i] <= 0) continue;
+    const int64_t a = start[i], b = (int64_t)start[i] + cnt[i];
+    for (int64_t lp = a / kvp::kPage; lp * kvp::kPage < b; ++lp) {
+      const int64_t lo = std::max<int64_t>(a, lp * kvp::kPage), hi = std::min<int64_t>(b, (lp + 1) * kvp::kPage);
+      runs->push_back(kvp::PageRun{i, (int32_t)lp, (int32_t)(lo - lp * kvp::kPage), (int32_t)(hi - lp * kvp::kPage),
+                                   first_src[i] + (lo - a)});
+    }
+  }
+}
+
+int upload_runs(const std::vector<kvp::PageRun>& runs, hipStream_t s, void** dev) {
+  *dev = nullptr;
+  if (runs.empty()) return KVP_OK;
+  const size_t n = runs.size() * sizeof(kvp::PageRun);
+  hipError_t e = hipMallocAsync(dev, n, s);
+  if (e != hipSuccess) return set_err(KVP_ENOMEM, "hipMallocAsync(%zu): %s", n, hipGetErrorString(e));
+  return staging().upload(*dev, runs.data(), n, s);
+}
+
+// Decode workspace: [metadata][partial accumulators][partial (m, l)].
+struct DecodeLayout {
+  kvp::DecodePlan plan;
+  Packer meta;
+  size_t off_wave = 0, off_group = 0, off_members = 0, off_part_base = 0, off_n_parts = 0, off_merge = 0;
+  size_t off_acc = 0, off_ml = 0, total = 0;
+};
+
+int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, const kvp_group_prefix* gp, int Hq,
+                  DecodeLayout* L) {
+  kvp::Status st = kvp::plan_decode(seq_lens, B, maxp, gp, Hq, pool->num_kv_heads, &L->plan);
+  if (!st.ok()) return from_status(st);
+  const auto& P = L->plan;
+  L->off_wave = L->meta.add(P.wave_items.data(), P.wave_items.size() * sizeof(kvp::DecodeItem));
+  L->off_group = L->meta.add(P.group_items.data(), P.group_items.size() * sizeof(kvp::DecodeItem));
+  L->off_members = L->meta.add(P.members.data(), P.members.size() * 4);
+  L->off_part_base = L->meta.add(P.part_base.data(), P.part_base.size() * 4);
+  L->off_n_parts = L->meta.add(P.n_parts.data(), P.n_parts.size() * 4);
+  L->off_merge = L->meta.add(P.merge_seqs.data(), P.merge_seqs.size() * 4);
+  L->off_acc = L->meta.size();
+  L->off_ml = L->off_acc + (((size_t)P.total_parts * Hq * pool->head_dim * 4 + 255) & ~size_t(255));
+  L->total = L->off_ml + (((size_t)P.total_parts * Hq * 8 + 255) & ~size_t(255));
+  return KVP_OK;
+}
+
+struct PrefillLayout {
+  kvp::PrefillPlan plan;
+  Packer meta;
+  size_t off_items = 0, off_ctx = 0, off_cuq = 0, total = 0;
+};
+
+int layout_prefill(kvp_pool_t pool, const int32_t* ctx_lens, const int32_t* cu_q, int B, int maxp, int Hq,
+                   PrefillLayout* L) {
+  kvp::Status st = kvp::plan_prefill(ctx_lens, cu_q, B, maxp, Hq, pool->num_kv_heads, &L->plan);
+  if (!st.ok()) return from_status(st);
+  L->off_items = L->meta.add(L->plan.items.data(), L->plan.items.size() * sizeof(kvp::PrefillItem));
+  L->off_ctx = L->meta.add(ctx_lens, (size_t)B * 4);
+  L->off_cuq = L->meta.add(cu_q, (size_t)(B + 1) * 4);
+  L->total = L->meta.size();
+  return KVP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* kvp_version(void) { return "kvpattn 0.1 (gfx950)"; }
+
+const char* kvp_last_error(void) { return g_last_error.c_str(); }
+
+const char* kvp_strerror(int code) {
+  switch (code) {
+    case KVP_OK: return "ok";
+    case KVP_EINVAL: return "invalid argument";
+    case KVP_ERANGE: return "length or page id out of range";
+    case KVP_EGROUP: return "inconsistent rollout-group prefix";
+    case KVP_ESHARED: return "write into a shared prefix page";
+    case KVP_EWORKSPACE: return "workspace too small";
+    case KVP_EUNSUPPORTED: return "unsupported shape or dtype";
+    case KVP_EHIP: return "HIP runtime error";
+    case KVP_ENOMEM: return "out of memory";
+    default: return "unknown error";
+  }
+}
+
+int kv_pool_create(kvp_pool_t* out, int num_layers, int num_pages, int page_size, int num_kv_heads, int head_dim,
+                   int dtype) {
+  if (!out) return set_err(KVP_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (num_layers <= 0 || num_pages <= 0 || num_kv_heads <= 0)
+    return set_err(KVP_EINVAL, "num_layers, num_pages and num_kv_heads must be positive");
+  if (page_size != kvp::kPage) return set_err(KVP_EUNSUPPORTED, "page_size %d (only 16 is supported)", page_size);
+  if (head_dim != 64 && head_dim != 128) return set_err(KVP_EUNSUPPORTED, "head_dim %d (64 or 128)", head_dim);
+  if (dtype != KVP_BF16) return set_err(KVP_EUNSUPPORTED, "dtype %d (only KVP_BF16)", dtype);
+  auto* p = new kvp_pool();
+  p->num_layers = num_layers;
+  p->num_pages = num_pages;
+  p->num_kv_heads = num_kv_heads;
+  p->head_dim = head_dim;
+  p->layer_bytes = (size_t)num_pages * num_kv_heads * 2 * kvp::kPage * head_dim * 2;
+  hipError_t e = hipGetDevice(&p->device);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&p->base), p->layer_bytes * num_layers);
+  if (e != hipSuccess) {
+    delete p;
+    return set_err(KVP_ENOMEM, "hipMalloc(pool of %zu bytes): %s", (size_t)0, hipGetErrorString(e));
+  }
+  e = hipMalloc(reinterpret_cast<void**>(&p->err), 256);
+  if (e == hipSuccess) e = kvp::launch_fill_zero(p->base, p->layer_bytes * num_layers, nullptr);
+  if (e == hipSuccess) e = kvp::launch_fill_zero(p->err, 256, nullptr);
+  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+  if (e != hipSuccess) {
+    (void)hipFree(p->base);
+    if (p->err) (void)hipFree(p->err);
+    delete p;
+    return hip_err(e, "kv_pool_create");
+  }
+  *out = p;
+  return KVP_OK;
+}
+
+int kv_pool_destroy(kvp_pool_t pool) {
+  if (!pool) return KVP_OK;
+  (void)hipDeviceSynchronize();
+  if (pool->base) (void)hipFree(pool->base);
+  if (pool->err) (void)hipFree(pool->err);
+  pool->base = nullptr;
+  delete pool;
+  return KVP_OK;
+}
+
+int kv_pool_reset(kvp_pool_t pool, void* stream) {
+  if (!pool_ok(pool)) return set_err(KVP_EINVAL, "pool is NULL or destroyed");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = kvp::launch_fill_zero(pool->base, pool->layer_bytes * pool->num_layers, s);
+  if (e == hipSuccess) e = kvp::launch_fill_zero(pool->err, 256, s);
+  return e == hipSuccess ? KVP_OK : hip_err(e, "kv_pool_reset");
+}
+
+int kv_pool_layer_ptr(kvp_pool_t pool, int layer, void** dev_ptr, size_t* bytes) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (dev_ptr) *dev_ptr = pool->base + (size_t)layer * pool->layer_bytes;
+  if (bytes) *bytes = pool->layer_bytes;
+  return KVP_OK;
+}
+
+int kv_pool_info(kvp_pool_t pool, int* num_layers, int* num_pages, int* num_kv_heads, int* head_dim) {
+  if (!pool_ok(pool)) return set_err(KVP_EINVAL, "pool is NULL or destroyed");
+  if (num_layers) *num_layers = pool->num_layers;
+  if (num_pages) *num_pages = pool->num_pages;
+  if (num_kv_heads) *num_kv_heads = pool->num_kv_heads;
+  if (head_dim) *head_dim = pool->head_dim;
+  return KVP_OK;
+}
+
+int kv_pool_device_error(kvp_pool_t pool, int* code) {
+  if (!pool_ok(pool) || !code) return set_err(KVP_EINVAL, "pool or code is NULL");
+  hipError_t e = hipDeviceSynchronize();
+  int v = 0;
+  if (e == hipSuccess) e = hipMemcpy(&v, pool->err, sizeof(int), hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemset(pool->err, 0, sizeof(int));
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_err(e, "kv_pool_device_error");
+  *code = v;
+  return KVP_OK;
+}
+
+int kv_append(kvp_pool_t pool, int layer, const void* k, const void* v, const int32_t* block_tables, int maxp,
+              const int32_t* start_pos, const int32_t* cu_new, int num_seqs, const kvp_group_prefix* gp,
+              void* stream) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (num_seqs < 0 || maxp < 0) return set_err(KVP_EINVAL, "num_seqs %d / maxp %d negative", num_seqs, maxp);
+  if (num_seqs == 0) return KVP_OK;
+  if (!start_pos || !cu_new || !block_tables) return set_err(KVP_EINVAL, "NULL metadata pointer");
+  if (cu_new[0] != 0) return set_err(KVP_EINVAL, "cu_new[0] = %d, must be 0", cu_new[0]);
+  std::vector<int32_t> cnt(num_seqs);
+  std::vector<int64_t> first(num_seqs);
+  for (int i = 0; i < num_seqs; ++i) {
+    cnt[i] = cu_new[i + 1] - cu_new[i];
+    first[i] = cu_new[i];
+    if (cnt[i] < 0) return set_err(KVP_EINVAL, "cu_new decreases at %d", i);
+    if (start_pos[i] < 0) return set_err(KVP_EINVAL, "start_pos[%d] = %d < 0", i, start_pos[i]);
+    if ((int64_t)start_pos[i] + cnt[i] > (int64_t)maxp * kvp::kPage)
+      return set_err(KVP_ERANGE, "sequence %d: positions up to %lld exceed maxp * 16 = %lld", i,
+                     (long long)start_pos[i] + cnt[i], (long long)maxp * kvp::kPage);
+  }
+  if (cu_new[num_seqs] > 0 && (!k || !v)) return set_err(KVP_EINVAL, "k or v is NULL");
+  if (gp) {
+    kvp::Status st = kvp::validate_group_prefix(nullptr, num_seqs, gp);
+    if (!st.ok()) return from_status(st);
+    if (gp->num_groups > 0)
+      for (int i = 0; i < num_seqs; ++i) {
+        const int g = gp->group_id[i];
+        if (g >= 0 && cnt[i] > 0 && (int64_t)start_pos[i] < (int64_t)gp->shared_pages[g] * kvp::kPage)
+          return set_err(KVP_ESHARED, "sequence %d would write position %d inside its group's %d shared pages", i,
+                         start_pos[i], gp->shared_pages[g]);
+      }
+  }
+  std::vector<kvp::PageRun> runs;
+  build_runs(start_pos, first.data(), cnt.data(), num_seqs, &runs);
+  if (runs.empty()) return KVP_OK;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  void* druns = nullptr;
+  rc = upload_runs(runs, s, &druns);
+  if (rc) return rc;
+  kvp::AppendArgs a{};
+  a.k = reinterpret_cast<const uint16_t*>(k);
+  a.v = reinterpret_cast<const uint16_t*>(v);
+  a.layer = const_cast<uint16_t*>(layer_ptr(pool, layer));
+  a.bt = block_tables;
+  a.runs = reinterpret_cast<const kvp::PageRun*>(druns);
+  a.n_runs = (int)runs.size();
+  a.maxp = maxp;
+  a.Hkv = pool->num_kv_heads;
+  a.num_pages = pool->num_pages;
+  a.err = pool->err;
+  hipError_t e = kvp::launch_append(a, pool->head_dim, s);
+  (void)hipFreeAsync(druns, s);
+  return e == hipSuccess ? KVP_OK : hip_err(e, "kv_append launch");
+}
+
+int kv_gather(kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp, const int32_t* lens, int num_seqs,
+              void* k_out, void* v_out, void* stream) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (num_seqs < 0 || maxp < 0) return set_err(KVP_EINVAL, "num_seqs / maxp negative");
+  if (num_seqs == 0) return KVP_OK;
+  if (!lens || !block_tables) return set_err(KVP_EINVAL, "NULL metadata pointer");
+  std::vector<int32_t> zero(num_seqs, 0);
+  std::vector<int64_t> first(num_seqs);
+  int64_t tot = 0;
+  for (int i = 0; i < num_seqs; ++i) {
+    if (lens[i] < 0 || (int64_t)lens[i] > (int64_t)maxp * kvp::kPage)
+      return set_err(KVP_ERANGE, "lens[%d] = %d outside [0, maxp*16]", i, lens[i]);
+    first[i] = tot;
+    tot += lens[i];
+  }
+  if (tot > 0 && (!k_out || !v_out)) return set_err(KVP_EINVAL, "k_out or v_out is NULL");
+  std::vector<kvp::PageRun> runs;
+  build_runs(zero.data(), first.data(), lens, num_seqs, &runs);
+  if (runs.empty()) return KVP_OK;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  void* druns = nullptr;
+  rc = upload_runs(runs, s, &druns);
+  if (rc) return rc;
+  kvp::GatherArgs a{};
+  a.k = reinterpret_cast<uint16_t*>(k_out);
+  a.v = reinterpret_cast<uint16_t*>(v_out);
+  a.layer = layer_ptr(pool, layer);
+  a.bt = block_tables;
+  a.runs = reinterpret_cast<const kvp::PageRun*>(druns);
+  a.n_runs = (int)runs.size();
+  a.maxp = maxp;
+  a.Hkv = pool->num_kv_heads;
+  a.num_pages = pool->num_pages;
+  a.err = pool->err;
+  hipError_t e = kvp::launch_gather(a, pool->head_dim, s);
+  (void)hipFreeAsync(druns, s);
+  return e == hipSuccess ? KVP_OK : hip_err(e, "kv_gather launch");
+}
+
+int paged_decode_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int num_seqs,
+                                const kvp_group_prefix* group_prefix, int num_q_heads, size_t* bytes) {
+  if (!pool_ok(pool) || !bytes) return set_err(KVP_EINVAL, "pool or bytes is NULL");
+  DecodeLayout L;
+  // The size query does not know maxp; lengths are range-checked again by paged_decode_attn.
+  int rc = layout_decode(pool, seq_lens, num_seqs, 1 << 28, group_prefix, num_q_heads, &L);
+  if (rc) return rc;
+  *bytes = L.total;
+  return KVP_OK;
+}
+
+int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
+                      const int32_t* seq_lens, int num_seqs, const kvp_group_prefix* group_prefix, int num_q_heads,
+                      float scale, void* out, int out_dtype, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
+  if (num_seqs == 0) return KVP_OK;
+  if (!q || !out || !block_tables || !seq_lens) return set_err(KVP_EINVAL, "NULL pointer argument");
+  if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
+  if (!std::isfinite(scale)) return set_err(KVP_EINVAL, "scale is not finite");
+  DecodeLayout L;
+  rc = layout_decode(pool, seq_lens, num_seqs, maxp, group_prefix, num_q_heads, &L);
+  if (rc) return rc;
+  if (!ws || ws_bytes < L.total)
+    return set_err(KVP_EWORKSPACE, "workspace of %zu bytes, %zu needed", ws ? ws_bytes : (size_t)0, L.total);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  unsigned char* w = reinterpret_cast<unsigned char*>(ws);
+  rc = staging().upload(w, L.meta.buf.data(), L.meta.buf.size(), s);
+  if (rc) return rc;
+  const auto& P = L.plan;
+  kvp::DecodeArgs a{};
+  a.q = reinterpret_cast<const uint16_t*>(q);
+  a.layer = layer_ptr(pool, layer);
+  a.bt = block_tables;
+  a.maxp = maxp;
+  a.members = reinterpret_cast<const int32_t*>(w + L.off_members);
+  a.part_base = reinterpret_cast<const int32_t*>(w + L.off_part_base);
+  a.part_acc = reinterpret_cast<float*>(w + L.off_acc);
+  a.part_ml = reinterpret_cast<float2*>(w + L.off_ml);
+  a.out = out;
+  a.out_f32 = out_dtype == KVP_F32;
+  a.Hq = num_q_heads;
+  a.Hkv = pool->num_kv_heads;
+  a.G = num_q_heads / pool->num_kv_heads;
+  a.num_pages = pool->num_pages;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.err = pool->err;
+  hipError_t e = hipSuccess;
+  if (!P.group_items.empty()) {
+    a.items = reinterpret_cast<const kvp::DecodeItem*>(w + L.off_group);
+    a.n_items = (int)P.group_items.size();
+    e = kvp::launch_decode_group(a, pool->head_dim, s);
+  }
+  if (e == hipSuccess && !P.wave_items.empty()) {
+    a.items = reinterpret_cast<const kvp::DecodeItem*>(w + L.off_wave);
+    a.n_items = (int)P.wave_items.size();
+    e = kvp::launch_decode_wave(a, pool->head_dim, s);
+  }
+  if (e == hipSuccess && !P.merge_seqs.empty()) {
+    kvp::MergeArgs m{};
+    m.merge_seqs = reinterpret_cast<const int32_t*>(w + L.off_merge);
+    m.n_merge = (int)P.merge_seqs.size();
+    m.part_base = a.part_base;
+    m.n_parts = reinterpret_cast<const int32_t*>(w + L.off_n_parts);
+    m.part_acc = a.part_acc;
+    m.part_ml = a.part_ml;
+    m.out = out;
+    m.out_f32 = a.out_f32;
+    m.Hq = num_q_heads;
+    e = kvp::launch_decode_merge(m, pool->head_dim, s);
+  }
+  return e == hipSuccess ? KVP_OK : hip_err(e, "paged_decode_attn launch");
+}
+
+int prefix_chunk_prefill_workspace_size(kvp_pool_t pool, const int32_t* ctx_lens, const int32_t* cu_q, int num_seqs,
+                                        int num_q_heads, size_t* bytes) {
+  if (!pool_ok(pool) || !bytes) return set_err(KVP_EINVAL, "pool or bytes is NULL");
+  PrefillLayout L;
+  int rc = layout_prefill(pool, ctx_lens, cu_q, num_seqs, 1 << 28, num_q_heads, &L);
+  if (rc) return rc;
+  *bytes = L.total;
+  return KVP_OK;
+}
+
+int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
+                              const int32_t* ctx_lens, const int32_t* cu_q, int num_seqs, int num_q_heads, float scale,
+                              void* out, int out_dtype, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
+  if (num_seqs == 0) return KVP_OK;
+  if (!q || !out || !block_tables || !ctx_lens || !cu_q) return set_err(KVP_EINVAL, "NULL pointer argument");
+  if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
+  if (!std::isfinite(scale)) return set_err(KVP_EINVAL, "scale is not finite");
+  PrefillLayout L;
+  rc = layout_prefill(pool, ctx_lens, cu_q, num_seqs, maxp, num_q_heads, &L);
+  if (rc) return rc;
+  if (L.plan.real_items == 0) return KVP_OK;
+  if (!ws || ws_bytes < L.total)
+    return set_err(KVP_EWORKSPACE, "workspace of %zu bytes, %zu needed", ws ? ws_bytes : (size_t)0, L.total);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  unsigned char* w = reinterpret_cast<unsigned char*>(ws);
+  rc = staging().upload(w, L.meta.buf.data(), L.meta.buf.size(), s);
+  if (rc) return rc;
+  kvp::PrefillArgs a{};
+  a.q = reinterpret_cast<const uint16_t*>(q);
+  a.layer = layer_ptr(pool, layer);
+  a.bt = block_tables;
+  a.maxp = maxp;
+  a.items = reinterpret_cast<const kvp::PrefillItem*>(w + L.off_items);
+  a.n_items = (int)L.plan.items.size();
+  a.ctx_lens = reinterpret_cast<const int32_t*>(w + L.off_ctx);
+  a.cu_q = reinterpret_cast<const int32_t*>(w + L.off_cuq);
+  a.out = out;
+  a.out_f32 = out_dtype == KVP_F32;
+  a.Hq = num_q_heads;
+  a.Hkv = pool->num_kv_heads;
+  a.G = num_q_heads / pool->num_kv_heads;
+  a.num_pages = pool->num_pages;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.err = pool->err;
+  hipError_t e = kvp::launch_prefill(a, pool->head_dim, s);
+  return e == hipSuccess ? KVP_OK : hip_err(e, "prefix_chunk_prefill_attn launch");
+}
+
+int kvp_check_tables(const int32_t* block_tables_host, int maxp, const int32_t* lens, int num_seqs, int num_pages,
+                     const kvp_group_prefix* gp) {
+  return from_status(kvp::check_tables(block_tables_host, maxp, lens, num_seqs, num_pages, gp));
+}
+
+int kvp_plan_decode(const int32_t* seq_lens, int num_seqs, const kvp_group_prefix* gp, int num_q_heads,
+                    int num_kv_heads, int32_t* items_out, int cap, int* n_items, int* n_partials,
+                    int* pages_per_split) {
+  kvp::DecodePlan P;
+  kvp::Status st = kvp::plan_decode(seq_lens, num_seqs, 1 << 28, gp, num_q_heads, num_kv_heads, &P);
+  if (!st.ok()) return from_status(st);
+  std::vector<kvp::DecodeItem> all(P.wave_items);
+  all.insert(all.end(), P.group_items.begin(), P.group_items.end());
+  for (int i = 0; i < (int)all.size() && i < cap && items_out; ++i) {
+    kvp::DecodeItem it = all[i];
+    if (it.kind == 0) it.mem_off = it.row;               // private: the member is the row itself
+    else it.mem_off = P.members[it.mem_off];             // prefix: first member of the (sub)group
+    std::memcpy(items_out + 8 * i, &it, sizeof(it));
+  }
+  if (n_items) *n_items = (int)all.size();
+  if (n_partials) *n_partials = P.total_parts;
+  if (pages_per_split) *pages_per_split = P.pages_per_split;
+  return KVP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,401 @@
+// Paged decode attention for prefix-shared rollout groups (gfx950).
+//
+// The work list (plan.cpp) splits every sequence's pages into ranges; each range of each KV head yields a
+// partial softmax state (running max m in log2 units, weight sum l, unnormalised accumulator acc) that
+// the merge kernel combines with a log-sum-exp rescale.  A rollout group's shared prompt pages (Sec. 3.1
+// group id g_r, Sec. 4.4 block-granular prefix reuse) form ranges of their own whose query columns are
+// every member's heads, so those pages are read from HBM once per group rather than once per sample.
+//
+// Tile shapes.  Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16: the 16 rows
+// are 16 tokens (8 of each of two pages), the 16 columns are query columns (member x head of one KV
+// head).  The score tile's register layout is exactly the layout of the P^T operand of the next product
+// O^T = V^T P^T (16 d-rows x 16 columns, k = 32 token slots of two pages), so probabilities never leave
+// registers.  The pool layout (kvp_layout.h) makes every K and V operand a contiguous 16-byte load.
+#include "kvp_kernels.h"
+#include "kvp_layout.h"
+
+namespace kvp {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                 c, 0, 0, 0);
+}
+
+__device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 v;
+  v[0] = (__bf16)lo;
+  v[1] = (__bf16)hi;
+  return __builtin_bit_cast(unsigned, v);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Per-lane online-softmax state for one query column and the 8 token slots this lane holds.
+template <int NT>
+struct SoftState {
+  f32x4 acc[NT];
+  float m;  // running max in log2 units (may lag the true max by < 8, see update)
+  float l;  // this lane's share of the weight sum (reduced over the 4 lane groups at the end)
+};
+
+// One two-page step: scale the 8 raw scores, mask invalid tokens, update the running max, accumulate
+// P^T V^T into acc.  `vv` are the lane's V^T operand tiles.  The max is only moved when a score exceeds
+// it by more than 2^8, so weights stay <= 256 (exact in bf16 range) and the rescale of acc is usually
+// skipped; the final normalisation uses the same max, so the result is unchanged.
+template <int NT>
+__device__ __forceinline__ void softmax_pv(SoftState<NT>& st, f32x4 sx, f32x4 sy, float scale_log2,
+                                           const bool (&ok)[8], bool masked, u32x4 (&vv)[NT]) {
+  float t[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    t[i] = sx[i] * scale_log2;
+    t[4 + i] = sy[i] * scale_log2;
+  }
+  if (masked) {
+    unsigned vm[4];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (!ok[j]) t[j] = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) vm[w] = (ok[2 * w] ? 0xFFFFu : 0u) | (ok[2 * w + 1] ? 0xFFFF0000u : 0u);
+#pragma unroll
+    for (int d = 0; d < NT; ++d)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) vv[d][w] &= vm[w];
+  }
+  float mx = fmaxf(fmaxf(fmaxf(t[0], t[1]), fmaxf(t[2], t[3])), fmaxf(fmaxf(t[4], t[5]), fmaxf(t[6], t[7])));
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const bool need = mx > st.m + 8.0f;
+  if (__any(need)) {
+    const float alpha = need ? fast_exp2(st.m - mx) : 1.0f;
+    st.m = need ? mx : st.m;
+    st.l *= alpha;
+#pragma unroll
+    for (int d = 0; d < NT; ++d) st.acc[d] *= alpha;
+  }
+  const float mr = (st.m == -INFINITY) ? 0.0f : st.m;
+  float p[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    p[j] = fast_exp2(t[j] - mr);
+    st.l += p[j];
+  }
+  u32x4 pp;
+  pp[0] = pack_bf16(p[0], p[1]);
+  pp[1] = pack_bf16(p[2], p[3]);
+  pp[2] = pack_bf16(p[4], p[5]);
+  pp[3] = pack_bf16(p[6], p[7]);
+#pragma unroll
+  for (int d = 0; d < NT; ++d) st.acc[d] = mfma16(vv[d], pp, st.acc[d]);
+}
+
+// Validity of the 8 tokens a lane holds in the step over pages (p, p+1): slots 8*(q4&1)+j of page
+// p + (q4>>1), i.e. tokens 4*(q4&1)+j (j<4) and 8+4*(q4&1)+j-4 (j>=4).
+__device__ __forceinline__ void lane_token_ok(int p, int q4, bool page_ok, int tok_end, bool (&ok)[8]) {
+  const int pos0 = (p + (q4 >> 1)) * 16 + (q4 & 1) * 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    ok[i] = page_ok && pos0 + i < tok_end;
+    ok[4 + i] = page_ok && pos0 + 8 + i < tok_end;
+  }
+}
+
+// Store one column's state: normalised output (slot < 0) or a partial for the merge kernel.
+template <int D, int NT>
+__device__ __forceinline__ void write_state(const DecodeArgs& a, const DecodeItem& it, const SoftState<NT>& st,
+                                            int seq, int head, int q4) {
+  if (it.slot < 0) {
+    const float inv = st.l > 0.0f ? 1.0f / st.l : 0.0f;
+    const int64_t o = ((int64_t)seq * a.Hq + head) * D + 4 * q4;
+#pragma unroll
+    for (int d = 0; d < NT; ++d) {
+      const f32x4 v = st.acc[d] * inv;
+      if (a.out_f32) {
+        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + o + 16 * d) = v;
+      } else {
+        uint2 u;
+        u.x = pack_bf16(v[0], v[1]);
+        u.y = pack_bf16(v[2], v[3]);
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + o + 16 * d) = u;
+      }
+    }
+  } else {
+    const int64_t pidx = (int64_t)a.part_base[seq] + it.slot;
+    float* pa = a.part_acc + (pidx * a.Hq + head) * D + 4 * q4;
+#pragma unroll
+    for (int d = 0; d < NT; ++d) *reinterpret_cast<f32x4*>(pa + 16 * d) = st.acc[d];
+    if (q4 == 0) a.part_ml[pidx * a.Hq + head] = make_float2(st.m, st.l);
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------
+// One wave per (item, KV head): private page ranges, and shared-prefix ranges of groups with <= 16
+// query columns.  Operands are loaded straight from HBM; each two-page step issues 2*D/32 K loads and
+// D/16 V loads of 16 bytes per lane (16 KB per wave at d = 128).
+// ---------------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void decode_wave_kernel(DecodeArgs a) {
+  constexpr int NS = D / 32;
+  constexpr int NT = D / 16;
+  constexpr int KB = 16 * D;
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int item = wid / a.Hkv;
+  const int kvh = wid - item * a.Hkv;
+  if (item >= a.n_items) return;
+  const DecodeItem it = a.items[item];
+  const int q4 = lane >> 4, c16 = lane & 15;
+  const int ncols = it.n_mem * a.G;
+  const bool col_ok = c16 < ncols;
+  int seq = 0, head = 0;
+  if (col_ok) {
+    const int m = c16 / a.G;
+    seq = a.members[it.mem_off + m];
+    head = kvh * a.G + (c16 - m * a.G);
+  }
+  u32x4 qt[NS];
+  {
+    const uint16_t* qr = a.q + ((int64_t)seq * a.Hq + head) * D;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qt[s] = col_ok ? ld16(qr + 8 * (4 * s + q4)) : u32x4{0u, 0u, 0u, 0u};
+  }
+  SoftState<NT> st;
+#pragma unroll
+  for (int d = 0; d < NT; ++d) st.acc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  st.m = -INFINITY;
+  st.l = 0.f;
+
+  const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
+  const uint16_t* hbase = a.layer + (int64_t)kvh * 2 * KB;
+  const int32_t* btr = a.bt + (int64_t)it.row * a.maxp;
+  const int k_off = (c16 & 7) * 8;
+  const int v_off = KB + ((q4 & 1) * 16 + c16) * 8;
+  bool bad = false;
+  for (int p = it.page_lo; p < it.page_hi; p += 2) {
+    const bool has_b = p + 1 < it.page_hi;
+    int ida = btr[p];
+    int idb = has_b ? btr[p + 1] : ida;
+    const bool va = (unsigned)ida < (unsigned)a.num_pages;
+    const bool vb = has_b && (unsigned)idb < (unsigned)a.num_pages;
+    bad |= !va || (has_b && !vb);
+    if (!va) ida = 0;
+    if (!vb) idb = ida;
+    const uint16_t* pa = hbase + (int64_t)ida * page_stride;
+    const uint16_t* pb = hbase + (int64_t)idb * page_stride;
+    const uint16_t* kp = (c16 < 8 ? pa : pb) + k_off;
+    const uint16_t* vp = (q4 < 2 ? pa : pb) + v_off;
+    u32x4 kx[NS], ky[NS], vv[NT];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      kx[s] = ld16(kp + (4 * s + q4) * 128);
+      ky[s] = ld16(kp + (4 * s + q4) * 128 + 64);
+    }
+#pragma unroll
+    for (int d = 0; d < NT; ++d) vv[d] = ld16(vp + d * 256);
+    f32x4 sx = {0.f, 0.f, 0.f, 0.f}, sy = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      sx = mfma16(kx[s], qt[s], sx);
+      sy = mfma16(ky[s], qt[s], sy);
+    }
+    const bool masked = !has_b || !va || !vb || (p + 2) * 16 > it.tok_end;
+    bool ok[8];
+    lane_token_ok(p, q4, q4 < 2 ? va : vb, it.tok_end, ok);
+    softmax_pv<NT>(st, sx, sy, a.scale_log2, ok, masked, vv);
+  }
+  if (bad && lane == 0) atomicCAS(a.err, 0, KVP_ERANGE);
+  st.l += __shfl_xor(st.l, 16);
+  st.l += __shfl_xor(st.l, 32);
+  if (!col_ok) return;
+  write_state<D, NT>(a, it, st, seq, head, q4);
+}
+
+// ---------------------------------------------------------------------------------------------------
+// One 4-wave workgroup per (shared-prefix item, KV head) for groups with 17..64 query columns (e.g. 8
+// samples x 8 heads).  Each two-page step is staged once in LDS by all 256 threads (double-buffered,
+// register-staged so the next step's HBM reads overlap this step's math); wave w then computes query
+// columns 16w..16w+15 from LDS.  The prefix pages therefore cross HBM once per group.
+// ---------------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void decode_group_kernel(DecodeArgs a) {
+  constexpr int NS = D / 32;
+  constexpr int NT = D / 16;
+  constexpr int KB = 16 * D;           // elements per K (or V) block
+  constexpr int PB = 4 * KB;           // bytes per (page, head): K + V blocks
+  constexpr int PAD = 128;             // keeps the two staged pages on different LDS banks
+  constexpr int SB = 2 * PB + PAD;
+  constexpr int NCH = 2 * PB / (256 * 16);
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2 * SB];
+
+  const int item = blockIdx.x / a.Hkv;
+  const int kvh = blockIdx.x - item * a.Hkv;
+  if (item >= a.n_items) return;
+  const DecodeItem it = a.items[item];
+  const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, q4 = lane >> 4, c16 = lane & 15;
+  const int ncols = it.n_mem * a.G;
+  const int col = wv * 16 + c16;
+  const bool wave_on = wv * 16 < ncols;
+  const bool col_ok = col < ncols;
+  int seq = 0, head = 0;
+  if (col_ok) {
+    const int m = col / a.G;
+    seq = a.members[it.mem_off + m];
+    head = kvh * a.G + (col - m * a.G);
+  }
+  u32x4 qt[NS];
+  {
+    const uint16_t* qr = a.q + ((int64_t)seq * a.Hq + head) * D;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qt[s] = col_ok ? ld16(qr + 8 * (4 * s + q4)) : u32x4{0u, 0u, 0u, 0u};
+  }
+  SoftState<NT> st;
+#pragma unroll
+  for (int d = 0; d < NT; ++d) st.acc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  st.m = -INFINITY;
+  st.l = 0.f;
+
+  const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
+  const uint16_t* hbase = a.layer + (int64_t)kvh * 2 * KB;
+  const int32_t* btr = a.bt + (int64_t)it.row * a.maxp;
+  bool bad = false;
+
+  // Stage pages (p, p+1) into registers; pages past the range or with invalid ids become zeros.
+  auto fetch = [&](int p, u32x4 (&r)[NCH]) {
+    const bool has_b = p + 1 < it.page_hi;
+    const int ida = btr[p];
+    const int idb = has_b ? btr[p + 1] : 0;
+    const bool va = (unsigned)ida < (unsigned)a.num_pages;
+    const bool vb = has_b && (unsigned)idb < (unsigned)a.num_pages;
+    bad |= !va || (has_b && !vb);
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      const int off = (k * 256 + tid) * 16;
+      const int pg = off / PB, inb = off - pg * PB;
+      const bool ok = pg == 0 ? va : vb;
+      const int id = pg == 0 ? ida : idb;
+      r[k] = ok ? ld16(reinterpret_cast<const unsigned char*>(hbase + (int64_t)id * page_stride) + inb)
+                : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto store = [&](int buf, const u32x4 (&r)[NCH]) {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      const int off = (k * 256 + tid) * 16;
+      const int pg = off / PB, inb = off - pg * PB;
+      *reinterpret_cast<u32x4*>(lds + buf * SB + pg * (PB + PAD) + inb) = r[k];
+    }
+  };
+
+  u32x4 r[NCH];
+  fetch(it.page_lo, r);
+  store(0, r);
+  __syncthreads();
+  int buf = 0;
+  for (int p = it.page_lo; p < it.page_hi; p += 2) {
+    const bool more = p + 2 < it.page_hi;
+    if (more) fetch(p + 2, r);
+    if (wave_on) {
+      const unsigned char* sb = lds + buf * SB;
+      const unsigned char* kp = sb + (c16 < 8 ? 0 : PB + PAD) + (c16 & 7) * 16;
+      const unsigned char* vp = sb + (q4 < 2 ? 0 : PB + PAD) + 2 * KB + ((q4 & 1) * 16 + c16) * 16;
+      u32x4 kx[NS], ky[NS], vv[NT];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        kx[s] = ld16(kp + (4 * s + q4) * 256);
+        ky[s] = ld16(kp + (4 * s + q4) * 256 + 128);
+      }
+#pragma unroll
+      for (int d = 0; d < NT; ++d) vv[d] = ld16(vp + d * 512);
+      f32x4 sx = {0.f, 0.f, 0.f, 0.f}, sy = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        sx = mfma16(kx[s], qt[s], sx);
+        sy = mfma16(ky[s], qt[s], sy);
+      }
+      const bool has_b = p + 1 < it.page_hi;
+      const bool va = (unsigned)btr[p] < (unsigned)a.num_pages;
+      const bool vb = has_b && (unsigned)btr[p + 1] < (unsigned)a.num_pages;
+      const bool masked = !has_b || !va || !vb || (p + 2) * 16 > it.tok_end;
+      bool ok[8];
+      lane_token_ok(p, q4, q4 < 2 ? va : vb, it.tok_end, ok);
+      softmax_pv<NT>(st, sx, sy, a.scale_log2, ok, masked, vv);
+    }
+    if (more) store(buf ^ 1, r);
+    __syncthreads();
+    buf ^= 1;
+  }
+  if (bad && tid == 0) atomicCAS(a.err, 0, KVP_ERANGE);
+  if (!wave_on) return;
+  st.l += __shfl_xor(st.l, 16);
+  st.l += __shfl_xor(st.l, 32);
+  if (!col_ok) return;
+  write_state<D, NT>(a, it, st, seq, head, q4);
+}
+
+// ---------------------------------------------------------------------------------------------------
+// Log-sum-exp merge: out = sum_j acc_j 2^(m_j - m) / sum_j l_j 2^(m_j - m), m = max_j m_j, in partial
+// order (fixed, so results are deterministic).  Empty partials (m = -inf, l = 0) carry zero weight; a
+// sequence with no partial gets a zero output.
+// ---------------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
+  const int seq = a.merge_seqs[blockIdx.x];
+  const int P = a.n_parts[seq];
+  const int64_t base = a.part_base[seq];
+  for (int e = threadIdx.x; e < a.Hq * D; e += 256) {
+    const int h = e / D, d = e - h * D;
+    float m = -INFINITY;
+    for (int j = 0; j < P; ++j) m = fmaxf(m, a.part_ml[(base + j) * a.Hq + h].x);
+    float o = 0.0f;
+    if (m != -INFINITY) {
+      float l = 0.0f, acc = 0.0f;
+      for (int j = 0; j < P; ++j) {
+        const float2 ml = a.part_ml[(base + j) * a.Hq + h];
+        const float w = fast_exp2(ml.x - m);
+        l += w * ml.y;
+        acc += w * a.part_acc[((base + j) * a.Hq + h) * D + d];
+      }
+      o = l > 0.0f ? acc / l : 0.0f;
+    }
+    const int64_t oi = ((int64_t)seq * a.Hq + h) * D + d;
+    if (a.out_f32) reinterpret_cast<float*>(a.out)[oi] = o;
+    else reinterpret_cast<__bf16*>(a.out)[oi] = (__bf16)o;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_decode_wave(const DecodeArgs& a, int D, hipStream_t s) {
+  const int64_t waves = (int64_t)a.n_items * a.Hkv;
+  if (waves == 0) return hipSuccess;
+  const dim3 grid((unsigned)((waves + 3) / 4));
+  if (D == 128) hipLaunchKernelGGL(decode_wave_kernel<128>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(decode_wave_kernel<64>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_group(const DecodeArgs& a, int D, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.n_items * a.Hkv;
+  if (blocks == 0) return hipSuccess;
+  if (D == 128) hipLaunchKernelGGL(decode_group_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(decode_group_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s) {
+  if (a.n_merge == 0) return hipSuccess;
+  if (D == 128) hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(a.n_merge), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(a.n_merge), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace kvp

@@ -1,0 +1,97 @@
+// Device-side definitions shared by the HIP kernels and the host launch code.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "kvp_plan.h"
+
+namespace kvp {
+
+// One run of tokens of one sequence that falls in one logical page (kv_append / kv_gather).
+struct PageRun {
+  int32_t row;      // block-table row
+  int32_t lpage;    // logical page
+  int32_t s_lo;     // first slot written / read
+  int32_t s_hi;     // one past the last slot
+  int64_t src0;     // token index (in the k / v arrays) of slot s_lo
+};
+static_assert(sizeof(PageRun) == 24, "PageRun is uploaded as raw bytes");
+
+struct AppendArgs {
+  const uint16_t* k;        // [T, Hkv, D]
+  const uint16_t* v;
+  uint16_t* layer;          // pool layer base
+  const int32_t* bt;        // [B, maxp]
+  const PageRun* runs;
+  int n_runs;
+  int maxp, Hkv, num_pages;
+  int* err;
+};
+
+struct GatherArgs {
+  uint16_t* k;              // [T, Hkv, D] out
+  uint16_t* v;
+  const uint16_t* layer;
+  const int32_t* bt;
+  const PageRun* runs;
+  int n_runs;
+  int maxp, Hkv, num_pages;
+  int* err;
+};
+
+struct DecodeArgs {
+  const uint16_t* q;        // [B, Hq, D] bf16
+  const uint16_t* layer;
+  const int32_t* bt;
+  int maxp;
+  const DecodeItem* items;
+  int n_items;
+  const int32_t* members;
+  const int32_t* part_base;
+  float* part_acc;          // [parts, Hq, D]
+  float2* part_ml;          // [parts, Hq] (running max in log2 units, sum of weights)
+  void* out;                // [B, Hq, D]
+  int out_f32;
+  int Hq, Hkv, G, num_pages;
+  float scale_log2;         // scale * log2(e)
+  int* err;
+};
+
+struct MergeArgs {
+  const int32_t* merge_seqs;
+  int n_merge;
+  const int32_t* part_base;
+  const int32_t* n_parts;
+  const float* part_acc;
+  const float2* part_ml;
+  void* out;
+  int out_f32;
+  int Hq;
+};
+
+struct PrefillArgs {
+  const uint16_t* q;        // [sum C, Hq, D]
+  const uint16_t* layer;
+  const int32_t* bt;
+  int maxp;
+  const PrefillItem* items;
+  int n_items;
+  const int32_t* ctx_lens;  // device copies
+  const int32_t* cu_q;
+  void* out;
+  int out_f32;
+  int Hq, Hkv, G, num_pages;
+  float scale_log2;
+  int* err;
+};
+
+hipError_t launch_append(const AppendArgs& a, int D, hipStream_t s);
+hipError_t launch_gather(const GatherArgs& a, int D, hipStream_t s);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_decode_wave(const DecodeArgs& a, int D, hipStream_t s);
+hipError_t launch_decode_group(const DecodeArgs& a, int D, hipStream_t s);
+hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s);
+hipError_t launch_prefill(const PrefillArgs& a, int D, hipStream_t s);
+
+}  // namespace kvp

@@ -1,0 +1,71 @@
+// Host-side planning for the paged attention kernels: validation of host metadata and the split-KV /
+// shared-prefix work lists the kernels consume.  Pure C++ (no HIP), so it builds and tests on a CPU.
+#pragma once
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/kvpattn.h"
+
+namespace kvp {
+
+constexpr int kPage = 16;
+constexpr int kMaxColsPerWave = 16;   // query columns one wave's MFMA tile holds (members x heads)
+constexpr int kMaxColsPerGroup = 64;  // query columns one shared-prefix workgroup holds (4 waves)
+
+// One unit of decode work: one KV head of it is processed by one wave (private, <= 16 query columns)
+// or one 4-wave workgroup (shared prefix, <= 64 query columns).  Mirrors kvp_plan_decode's 8 ints.
+struct DecodeItem {
+  int32_t kind;      // 0 = private range of one sequence, 1 = shared prefix of a group (or subgroup)
+  int32_t row;       // block-table row the pages are read from
+  int32_t page_lo;   // first logical page
+  int32_t page_hi;   // one past the last logical page
+  int32_t tok_end;   // tokens [0, tok_end) of the row are valid
+  int32_t mem_off;   // first entry in the member list (sequence ids owning the query columns)
+  int32_t n_mem;     // member count; query columns = n_mem * G
+  int32_t slot;      // partial index within each member's list, -1 = write the final output directly
+};
+static_assert(sizeof(DecodeItem) == 32, "DecodeItem is uploaded as raw bytes");
+
+struct DecodePlan {
+  std::vector<DecodeItem> wave_items;   // private items and prefix items with n_mem * G <= 16
+  std::vector<DecodeItem> group_items;  // prefix items with 16 < n_mem * G <= 64 (LDS-staged kernel)
+  std::vector<int32_t> members;         // member lists referenced by items
+  std::vector<int32_t> part_base;       // [B] first partial index of each sequence
+  std::vector<int32_t> n_parts;         // [B] partial count of each sequence
+  std::vector<int32_t> merge_seqs;      // sequences whose output the merge kernel writes (0 or >= 2 parts)
+  int32_t total_parts = 0;
+  int32_t pages_per_split = 0;
+};
+
+// Prefill: one 4-wave workgroup per (session, kv head, 128-row query tile).
+struct PrefillItem {
+  int32_t seq;       // session index (block-table row)
+  int32_t kvh;       // KV head
+  int32_t row0;      // first flattened query row (position * G + head-in-group) of the tile
+  int32_t pad;
+};
+static_assert(sizeof(PrefillItem) == 16, "PrefillItem is uploaded as raw bytes");
+
+struct PrefillPlan {
+  std::vector<PrefillItem> items;  // blockIdx order (XCD-aware, empty entries have seq = -1)
+  int64_t real_items = 0;
+};
+
+struct Status {
+  int code = KVP_OK;
+  std::string msg;
+  bool ok() const { return code == KVP_OK; }
+};
+
+Status validate_group_prefix(const int32_t* lens, int B, const kvp_group_prefix* gp);
+Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_prefix* gp, int Hq, int Hkv,
+                   DecodePlan* plan);
+Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int maxp, int Hq, int Hkv,
+                    PrefillPlan* plan);
+Status check_tables(const int32_t* bt, int maxp, const int32_t* lens, int B, int num_pages,
+                    const kvp_group_prefix* gp);
+
+constexpr int kPrefillRows = 128;  // flattened query rows per prefill workgroup
+
+}  // namespace kvp

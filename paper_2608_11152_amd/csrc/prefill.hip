@@ -1,0 +1,223 @@
+// Chunked prefill of a new turn over a cached history (Eq. 1 of the paper: a later agentic turn only
+// prefills its L - H uncached tokens; they attend to the cached H tokens and causally to each other).
+//
+// One 4-wave workgroup per (session, KV head, 128 flattened query rows).  Query rows are flattened as
+// position * G + head-in-group, so every K/V tile loaded serves all G query heads of its KV head.  Keys
+// stream through LDS in stages of 4 pages (64 keys), double-buffered through registers so the next
+// stage's HBM reads overlap this stage's MFMA work.  Wave w owns 32 query rows:
+//   S^T (64 keys x 32 rows) = K Q^T      v_mfma_f32_32x32x16_bf16, 2 key tiles x D/16 k-steps
+//   O^T (D x 32 rows)      += V^T P^T    the score tile's registers are the P^T operand (per page)
+// Masking is applied only to stages that reach past the wave's first query position (the diagonal).
+#include "kvp_kernels.h"
+#include "kvp_layout.h"
+
+namespace kvp {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                 c, 0, 0, 0);
+}
+
+__device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 v;
+  v[0] = (__bf16)lo;
+  v[1] = (__bf16)hi;
+  return __builtin_bit_cast(unsigned, v);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
+  constexpr int NS = D / 16;           // k-steps of the score product
+  constexpr int NDT = D / 32;          // 32-row d tiles of the output
+  constexpr int KB = 16 * D;           // elements per K (or V) block
+  constexpr int PB = 4 * KB;           // bytes per (page, head) block
+  constexpr int NPG = 4;               // pages per stage
+  constexpr int SB = NPG * PB;
+  constexpr int NCH = SB / (256 * 16);
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2 * SB];
+
+  const PrefillItem it = a.items[blockIdx.x];
+  if (it.seq < 0) return;
+  const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
+  const int G = a.G;
+  const int ctx = a.ctx_lens[it.seq];
+  const int q0 = a.cu_q[it.seq];
+  const int C = a.cu_q[it.seq + 1] - q0;
+  const int nrows = C * G;
+  const int f = it.row0 + wv * 32 + l32;  // this lane's query column (flattened row)
+  const bool row_ok = f < nrows;
+  const int fpos = (row_ok ? f : nrows - 1) / G;
+  const int hl = (row_ok ? f : nrows - 1) - fpos * G;
+  const int qpos = ctx + fpos;
+  const int n_keys = ctx + (min(nrows - 1, it.row0 + 127) / G) + 1;  // keys any row of the tile sees
+  const int wave_min_pos = ctx + min(it.row0 + wv * 32, nrows - 1) / G;
+  const int n_pages = (n_keys + 15) / 16;
+  const int n_stages = (n_keys + 63) / 64;
+
+  u32x4 qt[NS];
+  {
+    const uint16_t* qr = a.q + ((int64_t)(q0 + fpos) * a.Hq + it.kvh * G + hl) * D + 8 * g;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qt[s] = ld16(qr + 16 * s);
+  }
+  f32x16 acc[NDT];
+#pragma unroll
+  for (int d = 0; d < NDT; ++d) acc[d] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
+  const uint16_t* hbase = a.layer + (int64_t)it.kvh * 2 * KB;
+  const int32_t* btr = a.bt + (int64_t)it.seq * a.maxp;
+  bool bad = false;
+
+  // Stage `st` = logical pages 4*st .. 4*st+3.  Pages beyond the tile's keys, pages with invalid ids and
+  // token slots beyond n_keys in the last page are staged as zeros.
+  auto fetch = [&](int st, u32x4 (&r)[NCH]) {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      const int off = (k * 256 + tid) * 16;
+      const int pg = off / PB, inb = off - pg * PB;
+      const int lp = st * NPG + pg;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (lp < n_pages) {
+        const int id = btr[lp];
+        if ((unsigned)id < (unsigned)a.num_pages) {
+          v = ld16(reinterpret_cast<const unsigned char*>(hbase + (int64_t)id * page_stride) + inb);
+          const int valid = n_keys - lp * 16;  // tokens of this page inside the tile's key range
+          if (valid < 16) {
+            if (inb < 2 * KB) {
+              if (((inb >> 4) & 15) >= valid) v = u32x4{0u, 0u, 0u, 0u};
+            } else {
+              const int h = ((inb - 2 * KB) >> 8) & 1;  // V chunk holds slots 8h..8h+7
+#pragma unroll
+              for (int w = 0; w < 4; ++w) {
+                const unsigned lo = slot_token(8 * h + 2 * w) < valid ? 0xFFFFu : 0u;
+                const unsigned hi = slot_token(8 * h + 2 * w + 1) < valid ? 0xFFFF0000u : 0u;
+                v[w] &= lo | hi;
+              }
+            }
+          }
+        } else {
+          bad = true;
+        }
+      }
+      r[k] = v;
+    }
+  };
+  auto store = [&](int buf, const u32x4 (&r)[NCH]) {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) *reinterpret_cast<u32x4*>(lds + buf * SB + (k * 256 + tid) * 16) = r[k];
+  };
+
+  u32x4 r[NCH];
+  fetch(0, r);
+  store(0, r);
+  __syncthreads();
+  int buf = 0;
+  for (int st = 0; st < n_stages; ++st) {
+    const bool more = st + 1 < n_stages;
+    if (more) fetch(st + 1, r);
+    const unsigned char* sb = lds + buf * SB;
+    f32x16 S[2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      S[kk] = f32x16{};
+      const unsigned char* kp = sb + (2 * kk + (l32 >> 4)) * PB + (g * 16 + (l32 & 15)) * 16;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) S[kk] = mfma32(ld16(kp + s * 512), qt[s], S[kk]);
+    }
+    float t[32];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) t[kk * 16 + i] = S[kk][i] * a.scale_log2;
+    const int kbase = st * 64;
+    if (kbase + 63 > wave_min_pos) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = kbase + kk * 32 + 8 * (i >> 2) + 4 * g + (i & 3);
+          if (key > qpos) t[kk * 16 + i] = -INFINITY;
+        }
+    }
+    float mx = t[0];
+#pragma unroll
+    for (int i = 1; i < 32; ++i) mx = fmaxf(mx, t[i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const bool need = mx > m_run + 8.0f;
+    if (__any(need)) {
+      const float alpha = need ? fast_exp2(m_run - mx) : 1.0f;
+      m_run = need ? mx : m_run;
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < NDT; ++d) acc[d] *= alpha;
+    }
+    const float mr = (m_run == -INFINITY) ? 0.0f : m_run;
+    u32x4 pb[NPG];
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      float p[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        p[j] = fast_exp2(t[(pg >> 1) * 16 + (pg & 1) * 8 + j] - mr);
+        l_run += p[j];
+      }
+      pb[pg][0] = pack_bf16(p[0], p[1]);
+      pb[pg][1] = pack_bf16(p[2], p[3]);
+      pb[pg][2] = pack_bf16(p[4], p[5]);
+      pb[pg][3] = pack_bf16(p[6], p[7]);
+    }
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      const unsigned char* vp = sb + pg * PB + 2 * KB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 512;
+#pragma unroll
+      for (int d = 0; d < NDT; ++d) acc[d] = mfma32(ld16(vp + d * 1024), pb[pg], acc[d]);
+    }
+    if (more) store(buf ^ 1, r);
+    __syncthreads();
+    buf ^= 1;
+  }
+  if (bad) atomicCAS(a.err, 0, KVP_ERANGE);
+  l_run += __shfl_xor(l_run, 32);
+  if (!row_ok) return;
+  const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+  const int64_t o = ((int64_t)(q0 + fpos) * a.Hq + it.kvh * G + hl) * D + 4 * g;
+#pragma unroll
+  for (int d = 0; d < NDT; ++d)
+#pragma unroll
+    for (int t4 = 0; t4 < 4; ++t4) {
+      const int64_t oi = o + 32 * d + 8 * t4;
+      const float v0 = acc[d][4 * t4] * inv, v1 = acc[d][4 * t4 + 1] * inv;
+      const float v2 = acc[d][4 * t4 + 2] * inv, v3 = acc[d][4 * t4 + 3] * inv;
+      if (a.out_f32) {
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.out) + oi) = make_float4(v0, v1, v2, v3);
+      } else {
+        uint2 u;
+        u.x = pack_bf16(v0, v1);
+        u.y = pack_bf16(v2, v3);
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + oi) = u;
+      }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_prefill(const PrefillArgs& a, int D, hipStream_t s) {
+  if (a.n_items == 0) return hipSuccess;
+  if (D == 128) hipLaunchKernelGGL(prefill_kernel<128>, dim3(a.n_items), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(prefill_kernel<64>, dim3(a.n_items), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace kvp

@@ -1,0 +1,290 @@
+"""Thin Python binding of libkvpattn (ctypes).  Argument marshalling only: every step of the attention
+path runs in the HIP library; there is no fallback.  Device arrays are torch tensors on the GPU (torch
+provides device memory and streams), host metadata arrays are numpy int32.
+
+The names follow the C-ABI in include/kvpattn.h.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkvpattn.so")
+
+KVP_OK, KVP_EINVAL, KVP_ERANGE, KVP_EGROUP, KVP_ESHARED, KVP_EWORKSPACE, KVP_EUNSUPPORTED, KVP_EHIP, KVP_ENOMEM = \
+    0, -1, -2, -3, -4, -5, -6, -7, -8
+KVP_BF16, KVP_F32 = 0, 1
+PAGE = 16
+
+# Every symbol the header declares (kept in sync by a CPU test that parses include/kvpattn.h).
+EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_reset", "kv_pool_layer_ptr", "kv_pool_info",
+           "kv_pool_device_error", "kv_append", "kv_gather", "paged_decode_workspace_size", "paged_decode_attn",
+           "prefix_chunk_prefill_workspace_size", "prefix_chunk_prefill_attn", "kvp_check_tables",
+           "kvp_plan_decode", "kvp_strerror", "kvp_last_error", "kvp_version"]
+
+
+class KvpError(RuntimeError):
+    def __init__(self, code: int, where: str, detail: str):
+        super().__init__(f"{where}: {detail} (code {code})")
+        self.code = code
+
+
+class GroupPrefix(C.Structure):
+    _fields_ = [("group_id", C.POINTER(C.c_int32)), ("shared_pages", C.POINTER(C.c_int32)),
+                ("num_groups", C.c_int32)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load the built library.  Raises if it has not been built: there is no CPU fallback."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing; build it with `python -m paper_2608_11152_amd.build`")
+        L = C.CDLL(LIB_PATH)
+        p, i, vp, sz = C.c_void_p, C.c_int, C.c_void_p, C.c_size_t
+        i32p = C.POINTER(C.c_int32)
+        gpp = C.POINTER(GroupPrefix)
+        L.kv_pool_create.argtypes = [C.POINTER(p), i, i, i, i, i, i]
+        L.kv_pool_destroy.argtypes = [p]
+        L.kv_pool_reset.argtypes = [p, vp]
+        L.kv_pool_layer_ptr.argtypes = [p, i, C.POINTER(vp), C.POINTER(sz)]
+        L.kv_pool_info.argtypes = [p, C.POINTER(i), C.POINTER(i), C.POINTER(i), C.POINTER(i)]
+        L.kv_pool_device_error.argtypes = [p, C.POINTER(i)]
+        L.kv_append.argtypes = [p, i, vp, vp, vp, i, i32p, i32p, i, gpp, vp]
+        L.kv_gather.argtypes = [p, i, vp, i, i32p, i, vp, vp, vp]
+        L.paged_decode_workspace_size.argtypes = [p, i32p, i, gpp, i, C.POINTER(sz)]
+        L.paged_decode_attn.argtypes = [vp, p, i, vp, i, i32p, i, gpp, i, C.c_float, vp, i, vp, sz, vp]
+        L.prefix_chunk_prefill_workspace_size.argtypes = [p, i32p, i32p, i, i, C.POINTER(sz)]
+        L.prefix_chunk_prefill_attn.argtypes = [vp, p, i, vp, i, i32p, i32p, i, i, C.c_float, vp, i, vp, sz, vp]
+        L.kvp_check_tables.argtypes = [i32p, i, i32p, i, i, gpp]
+        L.kvp_plan_decode.argtypes = [i32p, i, gpp, i, i, i32p, i, C.POINTER(i), C.POINTER(i), C.POINTER(i)]
+        L.kvp_strerror.argtypes = [i]
+        L.kvp_strerror.restype = C.c_char_p
+        L.kvp_last_error.restype = C.c_char_p
+        L.kvp_version.restype = C.c_char_p
+        for name in EXPORTS:
+            if name not in ("kvp_strerror", "kvp_last_error", "kvp_version"):
+                getattr(L, name).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, where: str):
+    if rc != KVP_OK:
+        raise KvpError(rc, where, lib().kvp_last_error().decode())
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+class _GP:
+    """Keeps the numpy arrays of a group-prefix hint alive while the C struct points into them."""
+
+    def __init__(self, group_id, shared_pages):
+        self.gid = _i32(group_id)
+        self.sp = _i32(shared_pages)
+        self.s = GroupPrefix(_ptr(self.gid), _ptr(self.sp) if self.sp.size else None, len(self.sp))
+
+    def ref(self):
+        return C.byref(self.s)
+
+
+def group_prefix(group_id, shared_pages):
+    return _GP(group_id, shared_pages)
+
+
+def _gp_ref(gp):
+    if gp is None:
+        return None
+    if isinstance(gp, tuple):
+        gp = _GP(*gp)
+    return gp.ref()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return C.c_void_p(stream)
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _dptr(t) -> C.c_void_p:
+    return C.c_void_p(t.data_ptr() if t is not None else 0)
+
+
+class Pool:
+    """A paged KV pool owned by the library (kv_pool_create / kv_pool_destroy)."""
+
+    def __init__(self, num_layers: int, num_pages: int, num_kv_heads: int, head_dim: int, page_size: int = PAGE,
+                 dtype: int = KVP_BF16):
+        h = C.c_void_p()
+        _check(lib().kv_pool_create(C.byref(h), num_layers, num_pages, page_size, num_kv_heads, head_dim, dtype),
+               "kv_pool_create")
+        self.handle = h
+        self.num_layers, self.num_pages, self.num_kv_heads, self.head_dim = num_layers, num_pages, num_kv_heads, head_dim
+
+    def close(self):
+        if self.handle:
+            lib().kv_pool_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def reset(self, stream=None):
+        _check(lib().kv_pool_reset(self.handle, _stream(stream)), "kv_pool_reset")
+
+    def layer_ptr(self, layer: int = 0):
+        p, n = C.c_void_p(), C.c_size_t()
+        _check(lib().kv_pool_layer_ptr(self.handle, layer, C.byref(p), C.byref(n)), "kv_pool_layer_ptr")
+        return p.value, n.value
+
+    def layer_raw(self, layer: int = 0):
+        """A zero-copy int16 device view of one pool layer's raw bf16 bits (layout in include/kvpattn.h)."""
+        import torch
+        ptr, nbytes = self.layer_ptr(layer)
+
+        class _View:
+            __cuda_array_interface__ = {"shape": (nbytes // 2,), "typestr": "<i2", "data": (ptr, False),
+                                        "version": 3, "strides": None}
+        return torch.as_tensor(_View(), device="cuda")
+
+    def device_error(self) -> int:
+        c = C.c_int()
+        _check(lib().kv_pool_device_error(self.handle, C.byref(c)), "kv_pool_device_error")
+        return c.value
+
+
+def kv_pool_create(num_layers, num_pages, num_kv_heads, head_dim, page_size=PAGE, dtype=KVP_BF16) -> Pool:
+    return Pool(num_layers, num_pages, num_kv_heads, head_dim, page_size, dtype)
+
+
+def kv_pool_destroy(pool: Pool):
+    pool.close()
+
+
+def kv_pool_reset(pool: Pool, stream=None):
+    pool.reset(stream)
+
+
+def kv_pool_device_error(pool: Pool) -> int:
+    return pool.device_error()
+
+
+def kv_append(pool: Pool, layer, k, v, block_tables, start_pos, cu_new, group_prefix=None, stream=None):
+    """k, v: device bf16 [T, Hkv, d]; block_tables: device int32 [B, maxp]; start_pos, cu_new: host."""
+    sp, cu = _i32(start_pos), _i32(cu_new)
+    _check(lib().kv_append(pool.handle, layer, _dptr(k), _dptr(v), _dptr(block_tables), block_tables.shape[1],
+                           _ptr(sp), _ptr(cu), len(sp), _gp_ref(group_prefix), _stream(stream)), "kv_append")
+
+
+def kv_gather(pool: Pool, layer, block_tables, lens, stream=None):
+    import torch
+    ln = _i32(lens)
+    T = int(ln.sum())
+    shape = (T, pool.num_kv_heads, pool.head_dim)
+    k = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    v = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    _check(lib().kv_gather(pool.handle, layer, _dptr(block_tables), block_tables.shape[1], _ptr(ln), len(ln),
+                           _dptr(k), _dptr(v), _stream(stream)), "kv_gather")
+    return k, v
+
+
+def paged_decode_workspace_size(pool: Pool, seq_lens, num_q_heads, group_prefix=None) -> int:
+    sl = _i32(seq_lens)
+    n = C.c_size_t()
+    _check(lib().paged_decode_workspace_size(pool.handle, _ptr(sl), len(sl), _gp_ref(group_prefix), num_q_heads,
+                                             C.byref(n)), "paged_decode_workspace_size")
+    return n.value
+
+
+def paged_decode_attn(q, pool: Pool, layer, block_tables, seq_lens, group_prefix=None, scale=None, out=None,
+                      out_dtype=None, ws=None, stream=None):
+    """q: device bf16 [B, Hq, d]; block_tables: device int32 [B, maxp]; seq_lens: host int32 [B]."""
+    import torch
+    sl = _i32(seq_lens)
+    B, Hq, d = q.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=out_dtype or torch.float32, device=q.device)
+    od = KVP_F32 if out.dtype == torch.float32 else KVP_BF16
+    gpr = group_prefix if not isinstance(group_prefix, tuple) else _GP(*group_prefix)
+    if ws is None:
+        ws = torch.empty(max(1, paged_decode_workspace_size(pool, sl, Hq, gpr)), dtype=torch.uint8, device=q.device)
+    _check(lib().paged_decode_attn(_dptr(q), pool.handle, layer, _dptr(block_tables), block_tables.shape[1],
+                                   _ptr(sl), len(sl), _gp_ref(gpr), Hq, float(scale), _dptr(out), od, _dptr(ws),
+                                   ws.numel(), _stream(stream)), "paged_decode_attn")
+    return out
+
+
+def prefix_chunk_prefill_workspace_size(pool: Pool, ctx_lens, cu_q, num_q_heads) -> int:
+    cl, cq = _i32(ctx_lens), _i32(cu_q)
+    n = C.c_size_t()
+    _check(lib().prefix_chunk_prefill_workspace_size(pool.handle, _ptr(cl), _ptr(cq), len(cl), num_q_heads,
+                                                     C.byref(n)), "prefix_chunk_prefill_workspace_size")
+    return n.value
+
+
+def prefix_chunk_prefill_attn(q, pool: Pool, layer, block_tables, ctx_lens, cu_q, scale=None, out=None,
+                              out_dtype=None, ws=None, stream=None):
+    """q: device bf16 [sum C, Hq, d]; block_tables: device int32 [B, maxp]; ctx_lens, cu_q: host."""
+    import torch
+    cl, cq = _i32(ctx_lens), _i32(cu_q)
+    T, Hq, d = q.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if out is None:
+        out = torch.empty((T, Hq, d), dtype=out_dtype or torch.float32, device=q.device)
+    od = KVP_F32 if out.dtype == torch.float32 else KVP_BF16
+    if ws is None:
+        ws = torch.empty(max(1, prefix_chunk_prefill_workspace_size(pool, cl, cq, Hq)), dtype=torch.uint8,
+                         device=q.device)
+    _check(lib().prefix_chunk_prefill_attn(_dptr(q), pool.handle, layer, _dptr(block_tables), block_tables.shape[1],
+                                           _ptr(cl), _ptr(cq), len(cl), Hq, float(scale), _dptr(out), od, _dptr(ws),
+                                           ws.numel(), _stream(stream)), "prefix_chunk_prefill_attn")
+    return out
+
+
+def kvp_check_tables(block_tables_host, lens, num_pages, group_prefix=None) -> int:
+    """Host validation of a host copy of the block tables; returns the kvp_status code."""
+    bt = _i32(block_tables_host)
+    ln = _i32(lens)
+    return lib().kvp_check_tables(_ptr(bt), bt.shape[1], _ptr(ln), len(ln), num_pages, _gp_ref(group_prefix))
+
+
+def kvp_plan_decode(seq_lens, num_q_heads, num_kv_heads, group_prefix=None):
+    """The decode work plan (host only): returns (items [n, 8] int32, n_partials, pages_per_split)."""
+    sl = _i32(seq_lens)
+    n, parts, ch = C.c_int(), C.c_int(), C.c_int()
+    _check(lib().kvp_plan_decode(_ptr(sl), len(sl), _gp_ref(group_prefix), num_q_heads, num_kv_heads, None, 0,
+                                 C.byref(n), C.byref(parts), C.byref(ch)), "kvp_plan_decode")
+    items = np.zeros((max(1, n.value), 8), dtype=np.int32)
+    _check(lib().kvp_plan_decode(_ptr(sl), len(sl), _gp_ref(group_prefix), num_q_heads, num_kv_heads,
+                                 _ptr(items), n.value, C.byref(n), C.byref(parts), C.byref(ch)), "kvp_plan_decode")
+    return items[: n.value], parts.value, ch.value
+
+
+def kvp_strerror(code: int) -> str:
+    return lib().kvp_strerror(code).decode()
+
+
+def kvp_version() -> str:
+    return lib().kvp_version().decode()

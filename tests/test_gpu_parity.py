@@ -1,0 +1,331 @@
+"""GPU parity of the HIP path (through the C-ABI) against the CPU fp64 oracle, on reduced-size versions of
+every workload class (several tiles, ragged tails), plus the bit-exact properties of the paged layout."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_11152_amd import kvpattn as kp
+from paper_2608_11152_amd import workloads as W
+
+from gpu_helpers import GpuCase, assert_close, note, to_dev_bits
+
+pytestmark = pytest.mark.gpu
+
+DECODE_CASES = ["tiny", "rlvr_s", "rlhf_s", "agentic_s", "mixed_s", "rlvr_d64"]
+
+
+@pytest.fixture(scope="module")
+def cases():
+    return {}
+
+
+def get_case(cases, name):
+    if name not in cases:
+        note(f"setup {name}")
+        cases[name] = GpuCase(W.make_workload(name))
+    return cases[name]
+
+
+# ------------------------------------------------------------------------------------------------
+# kv_append: bit-exact round trip and the documented pool layout
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny", "mixed_s", "rlvr_d64"])
+def test_append_round_trip_bitwise(cases, name):
+    c = get_case(cases, name)
+    w = c.w
+    note(f"kv_gather {name}")
+    k, v = kp.kv_gather(c.pool, 0, c.bt, w.final_len)
+    import torch
+    torch.cuda.synchronize()
+    kb = k.view(torch.int16).cpu().numpy().view(np.uint16)
+    vb = v.view(torch.int16).cpu().numpy().view(np.uint16)
+    off = 0
+    for i in range(w.B):
+        n = int(w.final_len[i])
+        ek, ev = W.seq_kv_bits(w, c.vals, i)
+        assert np.array_equal(kb[off:off + n], ek), f"K of sequence {i}"
+        assert np.array_equal(vb[off:off + n], ev), f"V of sequence {i}"
+        off += n
+    assert c.pool.device_error() == kp.KVP_OK
+
+
+def _layout_index(D, t, c, which):
+    """Element offset inside a (page, head) block as documented in include/kvpattn.h."""
+    if which == 0:
+        return ((c // 8) * 16 + t) * 8 + c % 8
+    s = (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1)
+    return 16 * D + (((c // 16) * 2 + s // 8) * 16 + c % 16) * 8 + s % 8
+
+
+@pytest.mark.parametrize("name", ["tiny", "rlvr_d64"])
+def test_pool_raw_layout_matches_header(cases, name):
+    c = get_case(cases, name)
+    w = c.w
+    raw = c.pool.layer_raw(0).cpu().numpy().view(np.uint16).reshape(c.num_pages, w.Hkv, 2 * 16 * w.d)
+    pk, pv = c.oracle_pool()
+    D = w.d
+    t = np.arange(16)[:, None]
+    cc = np.arange(D)[None, :]
+    ik = _layout_index(D, t, cc, 0)
+    iv = _layout_index(D, t, cc, 1)
+    for page in np.unique(w.block_tables[w.block_tables >= 0])[:40]:
+        for h in range(w.Hkv):
+            assert np.array_equal(raw[page, h][ik], pk[page, h]), (page, h)
+            assert np.array_equal(raw[page, h][iv], pv[page, h]), (page, h)
+
+
+# ------------------------------------------------------------------------------------------------
+# decode parity
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", DECODE_CASES)
+def test_decode_parity_f32(cases, name):
+    c = get_case(cases, name)
+    note(f"decode {name} f32")
+    got = c.decode()
+    assert_close(got, c.oracle_decode(), f"decode {name}")
+    assert c.pool.device_error() == kp.KVP_OK
+
+
+@pytest.mark.parametrize("name", ["tiny", "rlvr_s", "mixed_s"])
+def test_decode_parity_bf16_out(cases, name):
+    import torch
+    c = get_case(cases, name)
+    note(f"decode {name} bf16")
+    got = c.decode(out_dtype=torch.bfloat16)
+    assert_close(got, c.oracle_decode(), f"decode {name} bf16-out")
+
+
+@pytest.mark.parametrize("name", ["rlvr_s", "rlhf_s", "mixed_s", "rlvr_d64"])
+def test_decode_shared_prefix_hint_vs_none(cases, name):
+    """The group-prefix hint reads shared pages once per group; the result must match the ungrouped run."""
+    c = get_case(cases, name)
+    note(f"decode {name} with / without group hint")
+    a = c.decode()
+    b = c.decode(group_prefix=None)
+    ref = c.oracle_decode()
+    assert_close(a, ref, f"{name} grouped")
+    assert_close(b, ref, f"{name} ungrouped")
+    assert_close(a, b.cpu().numpy().astype(np.float64), f"{name} grouped vs ungrouped")
+
+
+def test_decode_page_permutation_bitwise():
+    """Same logical content under a different physical page assignment: bitwise identical outputs."""
+    import torch
+    w = W.make_workload("mixed_s")
+    vals = W.make_values(w)
+    a = GpuCase(w, vals)
+    perm = np.random.default_rng(77).permutation(w.num_pages)
+    bt2 = np.where(w.block_tables >= 0, perm[np.maximum(w.block_tables, 0)], -1).astype(np.int32)
+    b = GpuCase(w, vals, block_tables=bt2)
+    note("decode permutation")
+    oa, ob = a.decode(), b.decode()
+    assert torch.equal(oa, ob)
+    pa, pb = a.prefill(), b.prefill()
+    assert torch.equal(pa, pb)
+
+
+def test_decode_deterministic(cases):
+    import torch
+    c = get_case(cases, "rlvr_s")
+    note("decode determinism")
+    assert torch.equal(c.decode(), c.decode())
+
+
+def test_decode_duplicated_prefix_pages_match_shared(cases):
+    """Members given private copies of the prompt pages (no sharing) give the shared-page result."""
+    w = W.make_workload("rlvr_d64")
+    vals = W.make_values(w)
+    shared = GpuCase(w, vals)
+    # Build a workload where every member owns copies of the prompt pages.
+    wd = W.make_workload("rlvr_d64")
+    extra = int(sum(w.shared_pages[g] * (np.sum(w.group_id == g) - 1) for g in range(w.num_groups)))
+    bt = w.block_tables.copy()
+    nxt = w.num_pages
+    seen = set()
+    for i in range(w.B):
+        g = int(w.group_id[i])
+        if g in seen:
+            for j in range(int(w.shared_pages[g])):
+                bt[i, j] = nxt
+                nxt += 1
+        seen.add(g)
+    assert nxt == w.num_pages + extra
+    wd.block_tables = bt
+    wd.shared_pages = np.zeros_like(w.shared_pages)
+    # every sequence appends its whole prefix into its own pages
+    import copy
+    ab = copy.deepcopy(w.setup_appends[1])
+    cnt = np.diff(ab.cu_new)
+    rows = []
+    for i in range(w.B):
+        rows.append(w.token_rows[i][: int(ab.start_pos[i]) + int(cnt[i])])
+    ab.start_pos = np.zeros(w.B, np.int32)
+    ab.cu_new = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int32)
+    ab.src_rows = np.concatenate(rows)
+    wd.setup_appends = [ab]
+    dup = GpuCase(wd, vals, num_pages=nxt)
+    note("decode duplicated prefix")
+    a, b = shared.decode(), dup.decode(group_prefix=None)
+    assert_close(b, shared.oracle_decode(), "duplicated prefix vs oracle")
+    assert_close(a, b.cpu().numpy().astype(np.float64), "shared vs duplicated")
+
+
+# ------------------------------------------------------------------------------------------------
+# prefill parity
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["agentic_s", "mixed_s"])
+def test_prefill_parity(cases, name):
+    c = get_case(cases, name)
+    note(f"prefill {name}")
+    got = c.prefill()
+    assert_close(got, c.oracle_prefill(), f"prefill {name}")
+    assert c.pool.device_error() == kp.KVP_OK
+
+
+def test_prefill_bf16_out(cases):
+    import torch
+    c = get_case(cases, "agentic_s")
+    note("prefill bf16")
+    assert_close(c.prefill(out_dtype=torch.bfloat16), c.oracle_prefill(), "prefill agentic_s bf16-out")
+
+
+@pytest.mark.parametrize("ctx,C,G", [(0, 37, 8), (0, 1, 8), (5, 1, 8), (16, 16, 4), (33, 130, 2), (1000, 3, 16),
+                                     (47, 64, 1)])
+def test_prefill_shapes(ctx, C, G):
+    """Causal ctx = 0, single-row chunks, page-aligned and ragged contexts, every GQA ratio."""
+    import torch
+    Hkv, d = 2, 128 if G != 16 else 64
+    Hq = G * Hkv
+    rng = np.random.default_rng(ctx * 1000 + C + G)
+    n = ctx + C
+    npg = (n + 15) // 16
+    num_pages = npg + 5
+    bt = rng.permutation(num_pages)[:npg].astype(np.int32)[None, :]
+    kvb = W.f32_to_bf16_bits(rng.standard_normal((n, 2, Hkv, d), dtype=np.float32))
+    qb = W.f32_to_bf16_bits(rng.standard_normal((C, Hq, d), dtype=np.float32))
+    pool = kp.Pool(1, num_pages, Hkv, d)
+    btd = torch.from_numpy(bt).cuda()
+    kvd = to_dev_bits(kvb)
+    note(f"prefill shape ctx={ctx} C={C} G={G}")
+    kp.kv_append(pool, 0, kvd[:, 0].contiguous(), kvd[:, 1].contiguous(), btd, [0], [0, n])
+    out = kp.prefix_chunk_prefill_attn(to_dev_bits(qb), pool, 0, btd, [ctx], [0, C], scale=0.09)
+    torch.cuda.synchronize()
+    ref = oracle.prefill_seq(qb, oracle.widen_bf16(kvb[:, 0]), oracle.widen_bf16(kvb[:, 1]), 0.09, ctx)
+    assert_close(out, ref, f"prefill ctx={ctx} C={C} G={G}")
+    # a chunk of one row is a decode step over ctx + 1 tokens
+    if C == 1:
+        dec = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, [n], scale=0.09)
+        torch.cuda.synchronize()
+        assert_close(dec, out.cpu().numpy().astype(np.float64), "decode == prefill of one row", 1e-5, 1e-6)
+
+
+# ------------------------------------------------------------------------------------------------
+# edge cases and errors
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("G,d", [(1, 128), (2, 64), (4, 128), (16, 64), (16, 128)])
+def test_decode_edge_lengths(G, d):
+    """Empty, single-token, page-aligned and ragged sequences, long sequences split many ways."""
+    import torch
+    lens = [0, 1, 2, 15, 16, 17, 31, 32, 33, 250, 4097, 0, 9000]
+    Hkv = 2
+    Hq = G * Hkv
+    rng = np.random.default_rng(G * 7 + d)
+    pages = [(n + 15) // 16 for n in lens]
+    maxp = max(pages)
+    num_pages = sum(pages) + 3
+    perm = rng.permutation(num_pages).astype(np.int32)
+    bt = np.full((len(lens), maxp), -1, np.int32)
+    o = 0
+    for i, p in enumerate(pages):
+        bt[i, :p] = perm[o:o + p]
+        o += p
+    T = sum(lens)
+    kvb = W.f32_to_bf16_bits(rng.standard_normal((T, 2, Hkv, d), dtype=np.float32))
+    qb = W.f32_to_bf16_bits(rng.standard_normal((len(lens), Hq, d), dtype=np.float32))
+    pool = kp.Pool(1, num_pages, Hkv, d)
+    btd = torch.from_numpy(bt).cuda()
+    kvd = to_dev_bits(kvb)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    note(f"decode edge lengths G={G} d={d}")
+    kp.kv_append(pool, 0, kvd[:, 0].contiguous(), kvd[:, 1].contiguous(), btd, np.zeros(len(lens), np.int32), cu)
+    out = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, lens, scale=0.1)
+    torch.cuda.synchronize()
+    pk, pv = oracle.new_pool(num_pages, Hkv, d)
+    oracle.append(pk, pv, kvb[:, 0], kvb[:, 1], bt, np.zeros(len(lens), np.int32), cu)
+    ref = oracle.decode(qb, pk, pv, bt, lens, 0.1)
+    assert_close(out, ref, f"edge lengths G={G} d={d}")
+    assert np.all(out[0].cpu().numpy() == 0) and np.all(out[11].cpu().numpy() == 0)
+
+
+def test_host_errors_enqueue_nothing(cases):
+    import torch
+    c = get_case(cases, "tiny")
+    w = c.w
+    q = to_dev_bits(c.vals.q)
+    sentinel = torch.full((w.B, w.Hq, w.d), 7.0, device="cuda")
+    too_long = w.decode_len.copy()
+    too_long[1] = w.maxp * 16 + 1
+    with pytest.raises(kp.KvpError) as e:
+        kp.paged_decode_attn(q, c.pool, 0, c.bt, too_long, out=sentinel)
+    assert e.value.code == kp.KVP_ERANGE
+    ws = torch.empty(8, dtype=torch.uint8, device="cuda")
+    with pytest.raises(kp.KvpError) as e:
+        kp.paged_decode_attn(q, c.pool, 0, c.bt, w.decode_len, out=sentinel, ws=ws)
+    assert e.value.code == kp.KVP_EWORKSPACE
+    with pytest.raises(kp.KvpError) as e:
+        kp.paged_decode_attn(q, c.pool, 3, c.bt, w.decode_len, out=sentinel)
+    assert e.value.code == kp.KVP_EINVAL
+    torch.cuda.synchronize()
+    assert torch.all(sentinel == 7.0)
+    # kv_append into a shared page is refused when the group hint is given
+    g = W.make_workload("rlvr_d64")
+    cg = get_case(cases, "rlvr_d64")
+    kv = cg.kv_dev[:1]
+    member = int(np.flatnonzero(g.group_id == 0)[1])
+    sp = np.zeros(g.B, np.int32)
+    cu = np.zeros(g.B + 1, np.int32)
+    cu[member + 1:] = 1
+    with pytest.raises(kp.KvpError) as e:
+        kp.kv_append(cg.pool, 0, kv[:, 0].contiguous(), kv[:, 1].contiguous(), cg.bt, sp, cu,
+                     group_prefix=kp.group_prefix(g.group_id, g.shared_pages))
+    assert e.value.code == kp.KVP_ESHARED
+
+
+def test_bad_page_id_is_skipped_and_reported():
+    """An out-of-pool page id in a device block table is never dereferenced: the kernels skip the page and
+    record KVP_ERANGE; outputs stay finite and equal attention over the remaining pages."""
+    import torch
+    w = W.make_workload("tiny")
+    c = GpuCase(w)
+    bt_bad = w.block_tables.copy()
+    bt_bad[3, 5] = w.num_pages + 1000
+    btd = torch.from_numpy(bt_bad).cuda()
+    note("decode with a bad page id")
+    out = kp.paged_decode_attn(to_dev_bits(c.vals.q), c.pool, 0, btd, w.decode_len, scale=w.scale)
+    torch.cuda.synchronize()
+    assert c.pool.device_error() == kp.KVP_ERANGE
+    assert c.pool.device_error() == kp.KVP_OK  # read-and-clear
+    o = out.cpu().numpy()
+    assert np.all(np.isfinite(o))
+    ref = c.oracle_decode()
+    assert_close(out[:3], ref[:3], "unaffected sequences")
+    # sequence 3 without page 5: attention over its other tokens
+    pk, pv = c.oracle_pool()
+    k, v = oracle.gather(pk, pv, w.block_tables[3], int(w.decode_len[3]))
+    keep = np.ones(len(k), bool)
+    keep[5 * 16:6 * 16] = False
+    exp = oracle.decode_seq(c.vals.q[3], k[keep], v[keep], w.scale)
+    assert_close(out[3:4], exp[None], "sequence with the skipped page")
+
+
+def test_pool_reset_zeroes(cases):
+    import torch
+    w = W.make_workload("tiny")
+    c = GpuCase(w)
+    c.pool.reset()
+    torch.cuda.synchronize()
+    assert bool(torch.all(c.pool.layer_raw(0) == 0))
