@@ -1,0 +1,257 @@
+"""Benchmark of the prefix-shared paged-KV attention path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload mixed] [--no-cpu-baseline]
+
+Workload (default): the mixed rollout step — 40 sessions (2 RLVR groups x 8 samples, 6 RLHF groups x 2,
+12 agentic sessions with 32k-128k cached history) in a 1.5M-token pool of randomly permuted pages.
+One step = kv_append of every session's new tokens (40 decode tokens + 8 agentic 2048-token chunks),
+paged_decode_attn for all 40 sessions (shared prompt pages read once per group, split-KV + LSE merge),
+then prefix_chunk_prefill_attn for the 8 chunks over their cached histories.  Inputs are synthetic
+(seeded N(0,1) bf16 values), resident in HBM before timing starts.  Each step first overwrites a 512 MB
+buffer so that no KV read can hit the 256 MB Infinity Cache left warm by the previous step (in a serving
+engine the rest of the model runs between two attention calls).
+
+Prints one JSON line.  `value` is the metric: effective decode KV bandwidth (algorithmic bytes of the
+paged_decode_attn call / its GPU time).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "paged decode-attn effective KV GB/s (% HBM peak) + decode tokens/s, mixed batch"
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+WORKLOAD_TEXT = {
+    "mixed": "mixed step: 40 sessions (16 RLVR in 2 groups x 8, 12 RLHF in 6 groups x 2, 12 agentic), "
+             "1.5M-token pool of permuted 16-token pages, decode for all 40 + 2048-token prefill chunks "
+             "for 8 agentic sessions; GQA 32/4, d=128, bf16",
+    "rlvr": "RLVR decode: 64 groups x 8 samples, shared prompt U[128,1024], private U[1k,16k]; GQA 32/4, d=128",
+    "rlhf": "RLHF decode: 128 groups x 2 samples, lognormal prompt/response (median 1k); GQA 32/4, d=128",
+    "agentic": "agentic turn: 32 sessions, history U[32k,128k], 2048-token chunk prefill + 1 decode; "
+               "GQA 32/4, d=128",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mixed", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle baseline sample")
+    ap.add_argument("--no-flush", action="store_true", help="do not evict the Infinity Cache between steps")
+    return ap.parse_args()
+
+
+def decode_algorithmic_bytes(w) -> int:
+    """KV bytes of every cached token decode reads, each group's shared pages counted once, plus Q, O
+    (bf16) and the block-table entries referenced."""
+    kv = w.unique_decode_tokens() * w.Hkv * w.d * 2 * 2
+    dec = w.decode_len > 0
+    qo = int(dec.sum()) * w.Hq * w.d * 2 * 2
+    pages = 0
+    for i in range(w.B):
+        n = int(w.decode_len[i])
+        if n:
+            g = int(w.group_id[i])
+            pages += (n + 15) // 16 - (int(w.shared_pages[g]) if g >= 0 else 0)
+    for g in range(w.num_groups):
+        if np.any((w.group_id == g) & dec):
+            pages += int(w.shared_pages[g])
+    return kv + qo + 4 * pages
+
+
+def prefill_algorithmic_bytes(w) -> int:
+    """Unique bytes the prefill must touch: each session's KV up to its last chunk token, Q and O."""
+    toks = int((w.prefill_ctx + w.prefill_chunk).sum())
+    return toks * w.Hkv * w.d * 4 + int(w.prefill_chunk.sum()) * w.Hq * w.d * 4
+
+
+def cpu_baseline(w, vals, budget_s: float):
+    """Time the CPU fp64 oracle (as it stands) on a bounded sample of the same decode workload."""
+    import oracle
+    from paper_2608_11152_amd import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = None
+    order = [i for i in range(w.B) if w.decode_len[i] > 0]
+    order.sort(key=lambda i: int(w.decode_len[i]))  # shortest first: many sessions within the budget
+    q_all = W.to_numpy_bits(vals.q)
+    done_bytes, done_tok, secs, n_seq = 0, 0, 0.0, 0
+    for i in order:
+        n = int(w.decode_len[i])
+        k, v = W.seq_kv_bits(w, vals, i, n)
+        t0 = time.perf_counter()
+        oracle.decode_seq(q_all[i], oracle.widen_bf16(k), oracle.widen_bf16(v), w.scale)
+        secs += time.perf_counter() - t0
+        done_bytes += n * w.Hkv * w.d * 4
+        done_tok += 1
+        n_seq += 1
+        if secs >= budget_s:
+            break
+    return {
+        "value": round(done_bytes / secs / 1e9, 4), "unit": "GB/s", "cores": blas_threads or os.cpu_count(),
+        "kind": "oracle",
+        "sample": f"numpy fp64 oracle decode of {n_seq}/{len(order)} sessions of the same workload "
+                  f"(shortest first, {done_bytes / 1e9:.3f} GB of logical KV, contiguous per-sequence K/V), "
+                  f"{secs:.1f} s; decode tokens/s = {done_tok / secs:.3f}; os.cpu_count()={os.cpu_count()}, "
+                  f"affinity={len(os.sched_getaffinity(0))}, blas_threads={blas_threads}",
+        "decode_tokens_per_s": round(done_tok / secs, 4),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is design-only "
+                                   "(see the sharding section of DESIGN.md)", "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+
+    from paper_2608_11152_amd import kvpattn as kp
+    from paper_2608_11152_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.make_workload(args.workload)
+    vals = W.make_values(w, values="torch", device=dev)
+    gp = kp.group_prefix(w.group_id, w.shared_pages) if w.num_groups else None
+    pool = kp.Pool(1, w.num_pages, w.Hkv, w.d)
+    bt = torch.from_numpy(w.block_tables).to(dev)
+
+    def append_batch(ab):
+        rows = torch.from_numpy(ab.src_rows).to(dev)
+        return (vals.kv[rows, 0].contiguous(), vals.kv[rows, 1].contiguous(), ab)
+
+    for ab in w.setup_appends:
+        k, v, _ = append_batch(ab)
+        kp.kv_append(pool, 0, k, v, bt, ab.start_pos, ab.cu_new, group_prefix=gp if ab.use_group_prefix else None)
+        del k, v
+    step_batches = [append_batch(ab) for ab in w.step_appends]
+    has_prefill = len(w.prefill_seqs) > 0
+    dec_ws = torch.empty(kp.paged_decode_workspace_size(pool, w.decode_len, w.Hq, gp), dtype=torch.uint8, device=dev)
+    dec_out = torch.empty((w.B, w.Hq, w.d), dtype=torch.bfloat16, device=dev)
+    if has_prefill:
+        s0, s1 = int(w.prefill_seqs[0]), int(w.prefill_seqs[-1]) + 1
+        cu_q = w.cu_q()
+        pf_ws = torch.empty(max(1, kp.prefix_chunk_prefill_workspace_size(pool, w.prefill_ctx, cu_q, w.Hq)),
+                            dtype=torch.uint8, device=dev)
+        pf_out = torch.empty((int(cu_q[-1]), w.Hq, w.d), dtype=torch.bfloat16, device=dev)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if not args.no_flush:
+            flush.fill_(1)
+        if ev:
+            ev[0].record(stream)
+        for k, v, ab in step_batches:
+            kp.kv_append(pool, 0, k, v, bt, ab.start_pos, ab.cu_new, group_prefix=gp if ab.use_group_prefix else None)
+        if ev:
+            ev[1].record(stream)
+        kp.paged_decode_attn(vals.q, pool, 0, bt, w.decode_len, group_prefix=gp, scale=w.scale, out=dec_out,
+                             ws=dec_ws)
+        if ev:
+            ev[2].record(stream)
+        if has_prefill:
+            kp.prefix_chunk_prefill_attn(vals.qp, pool, 0, bt[s0:s1], w.prefill_ctx, cu_q, scale=w.scale,
+                                         out=pf_out, ws=pf_ws)
+        if ev:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    err = pool.device_error()
+    if err != kp.KVP_OK:
+        raise RuntimeError(f"device error {err} during the benchmark")
+    t_app = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    t_dec = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    t_pf = np.array([e[2].elapsed_time(e[3]) for e in evs])
+
+    # Plain device copy of 1 GiB (2 GiB of HBM traffic): the bandwidth a streaming kernel reaches here.
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(5):
+        dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * (1 << 30) / (c0.elapsed_time(c1) / 1e3) / 1e9
+    del src, dst
+
+    dec_bytes = decode_algorithmic_bytes(w)
+    dec_s = float(np.mean(t_dec)) / 1e3
+    dec_gbs = dec_bytes / dec_s / 1e9
+    n_dec = int((w.decode_len > 0).sum())
+    res = {
+        "metric": METRIC,
+        "value": round(dec_gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "sessions": w.B, "decode_sessions": n_dec,
+                   "prefill_chunks": int(len(w.prefill_seqs)), "pool_pages": w.num_pages,
+                   "unique_decode_tokens": w.unique_decode_tokens(),
+                   "logical_decode_tokens": w.logical_decode_tokens(), "seed": w.seed},
+        "decode_hbm_peak_frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+        "decode_tokens_per_s": round(n_dec / dec_s, 1),
+        "decode_ms": {"mean": round(float(np.mean(t_dec)), 4), "p10": round(float(np.percentile(t_dec, 10)), 4),
+                      "p90": round(float(np.percentile(t_dec, 90)), 4)},
+        "append_ms": round(float(np.mean(t_app)), 4),
+        "hbm_copy_gbs": round(copy_gbs, 1),
+        "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "paged_decode_attn (shared-prefix + split-KV partial kernels and LSE merge)",
+                     "algorithmic_bytes_per_launch": dec_bytes},
+    }
+    if has_prefill:
+        pf_s = float(np.mean(t_pf)) / 1e3
+        flops = w.prefill_flops()
+        res["prefill_ms"] = {"mean": round(float(np.mean(t_pf)), 4), "p10": round(float(np.percentile(t_pf, 10)), 4),
+                             "p90": round(float(np.percentile(t_pf, 90)), 4)}
+        res["prefill_tflops"] = round(flops / pf_s / 1e12, 2)
+        res["roofline_prefill"] = {"bound": "mfma", "achieved": round(flops / pf_s / 1e12, 2),
+                                   "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                   "frac": round(flops / pf_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                                   "kernel": "prefix_chunk_prefill_attn", "algorithmic_flops_per_launch": flops,
+                                   "algorithmic_bytes_per_launch": prefill_algorithmic_bytes(w)}
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, vals, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+    pool.close()
+
+
+if __name__ == "__main__":
+    main()

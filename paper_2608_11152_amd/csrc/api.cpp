@@ -460,6 +460,7 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
     m.out = out;
     m.out_f32 = a.out_f32;
     m.Hq = num_q_heads;
+    m.Hkv = pool->num_kv_heads;
     e = kvp::launch_decode_merge(m, pool->head_dim, s);
   }
   return e == hipSuccess ? KVP_OK : hip_err(e, "paged_decode_attn launch");

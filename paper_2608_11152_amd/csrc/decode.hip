@@ -344,31 +344,62 @@ __global__ __launch_bounds__(256) void decode_group_kernel(DecodeArgs a) {
 // ---------------------------------------------------------------------------------------------------
 // Log-sum-exp merge: out = sum_j acc_j 2^(m_j - m) / sum_j l_j 2^(m_j - m), m = max_j m_j, in partial
 // order (fixed, so results are deterministic).  Empty partials (m = -inf, l = 0) carry zero weight; a
-// sequence with no partial gets a zero output.
+// sequence with no partial gets a zero output.  One workgroup per (sequence, KV head): the G heads' max
+// and weight sum are reduced once into LDS (16 threads per head), then every thread accumulates four
+// consecutive output dims with 16-byte loads of the partial accumulators.
 // ---------------------------------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
-  const int seq = a.merge_seqs[blockIdx.x];
+  __shared__ float s_m[16], s_inv[16];
+  const int seq = a.merge_seqs[blockIdx.x / a.Hkv];
+  const int kvh = blockIdx.x - (blockIdx.x / a.Hkv) * a.Hkv;
+  const int G = a.Hq / a.Hkv;
   const int P = a.n_parts[seq];
   const int64_t base = a.part_base[seq];
-  for (int e = threadIdx.x; e < a.Hq * D; e += 256) {
-    const int h = e / D, d = e - h * D;
+  const int tid = threadIdx.x;
+  {
+    const int hh = tid >> 4, r = tid & 15;
+    const int h = kvh * G + hh;
     float m = -INFINITY;
-    for (int j = 0; j < P; ++j) m = fmaxf(m, a.part_ml[(base + j) * a.Hq + h].x);
-    float o = 0.0f;
-    if (m != -INFINITY) {
-      float l = 0.0f, acc = 0.0f;
-      for (int j = 0; j < P; ++j) {
+    if (hh < G)
+      for (int j = r; j < P; j += 16) m = fmaxf(m, a.part_ml[(base + j) * a.Hq + h].x);
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 16));
+    float l = 0.0f;
+    if (hh < G && m != -INFINITY)
+      for (int j = r; j < P; j += 16) {
         const float2 ml = a.part_ml[(base + j) * a.Hq + h];
-        const float w = fast_exp2(ml.x - m);
-        l += w * ml.y;
-        acc += w * a.part_acc[((base + j) * a.Hq + h) * D + d];
+        l += fast_exp2(ml.x - m) * ml.y;
       }
-      o = l > 0.0f ? acc / l : 0.0f;
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) l += __shfl_xor(l, o, 16);
+    if (hh < G && r == 0) {
+      s_m[hh] = m;
+      s_inv[hh] = (m != -INFINITY && l > 0.0f) ? 1.0f / l : 0.0f;
     }
-    const int64_t oi = ((int64_t)seq * a.Hq + h) * D + d;
-    if (a.out_f32) reinterpret_cast<float*>(a.out)[oi] = o;
-    else reinterpret_cast<__bf16*>(a.out)[oi] = (__bf16)o;
+  }
+  __syncthreads();
+  constexpr int V4 = D / 4;  // float4 per head row
+  for (int e = tid; e < G * V4; e += 256) {
+    const int hh = e / V4, d4 = e - hh * V4;
+    const int h = kvh * G + hh;
+    const float m = s_m[hh], inv = s_inv[hh];
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    if (inv > 0.0f)
+      for (int j = 0; j < P; ++j) {
+        const float w = fast_exp2(a.part_ml[(base + j) * a.Hq + h].x - m);
+        acc += w * *reinterpret_cast<const f32x4*>(a.part_acc + ((base + j) * a.Hq + h) * D + 4 * d4);
+      }
+    acc *= inv;
+    const int64_t oi = ((int64_t)seq * a.Hq + h) * D + 4 * d4;
+    if (a.out_f32) {
+      *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + oi) = acc;
+    } else {
+      uint2 u;
+      u.x = pack_bf16(acc[0], acc[1]);
+      u.y = pack_bf16(acc[2], acc[3]);
+      *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + oi) = u;
+    }
   }
 }
 
@@ -393,8 +424,9 @@ hipError_t launch_decode_group(const DecodeArgs& a, int D, hipStream_t s) {
 
 hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s) {
   if (a.n_merge == 0) return hipSuccess;
-  if (D == 128) hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(a.n_merge), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(a.n_merge), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)((int64_t)a.n_merge * a.Hkv));
+  if (D == 128) hipLaunchKernelGGL(decode_merge_kernel<128>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

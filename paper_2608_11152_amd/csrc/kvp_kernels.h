@@ -67,7 +67,7 @@ struct MergeArgs {
   const float2* part_ml;
   void* out;
   int out_f32;
-  int Hq;
+  int Hq, Hkv;
 };
 
 struct PrefillArgs {

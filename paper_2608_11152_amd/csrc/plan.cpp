@@ -3,6 +3,7 @@
 // page ids, so GPU results are bitwise reproducible under any page permutation.
 #include <algorithm>
 #include <cstdio>
+#include <cstdlib>
 #include <numeric>
 
 #include "kvp_plan.h"
@@ -41,6 +42,17 @@ Status validate_group_prefix(const int32_t* lens, int B, const kvp_group_prefix*
                   i, lens[i], gp->shared_pages[g]);
   }
   return {};
+}
+
+// Target number of decode waves per call.  KVP_DECODE_WAVES overrides the default for tuning sweeps;
+// the plan stays a pure function of its inputs for a given value.
+static int64_t decode_target_waves() {
+  static const int64_t v = [] {
+    const char* e = std::getenv("KVP_DECODE_WAVES");
+    const long x = e ? std::strtol(e, nullptr, 10) : 0;
+    return x > 0 ? (int64_t)x : (int64_t)4096;
+  }();
+  return v;
 }
 
 // Split [lo, hi) pages into nearly equal ranges of at most `ch` pages; interior boundaries are even so
@@ -87,8 +99,9 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   for (int i = 0; i < B; ++i)
     if (seq_lens[i] > 0 && shared_of(i) > 0) mem[gp->group_id[i]].push_back(i);
 
-  // Pages per split: aim for about 16384 waves (64 per CU over 256 CUs) so that equal-sized splits
-  // balance across the chip; never below 16 pages (256 tokens) so partial traffic stays a few percent.
+  // Pages per split: aim for about decode_target_waves() waves (several rounds of the ~12 waves per CU
+  // that fit on 256 CUs) so equal-sized splits balance across the chip; never below 32 pages (512 tokens),
+  // so a split's partial (G x d fp32 written, then read by the merge) stays within ~2% of its KV bytes.
   int64_t page_heads = 0;
   for (int i = 0; i < B; ++i) {
     const int np = (seq_lens[i] + kPage - 1) / kPage;
@@ -96,8 +109,9 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   }
   for (int g = 0; g < NG; ++g)
     if (!mem[g].empty()) page_heads += (int64_t)gp->shared_pages[g] * Hkv;
-  int64_t ch = (page_heads + 16383) / 16384;
-  ch = std::max<int64_t>(16, std::min<int64_t>(1024, ch));
+  const int64_t waves = decode_target_waves();
+  int64_t ch = (page_heads + waves - 1) / waves;
+  ch = std::max<int64_t>(32, std::min<int64_t>(1024, ch));
   ch = (ch + 1) & ~1;
   plan->pages_per_split = (int)ch;
 
