@@ -99,6 +99,35 @@ Staging& staging() {
   return *s;
 }
 
+// A library-owned side stream per device (default priority) onto which paged_decode_attn forks the
+// LDS-staged shared-prefix kernel so that it runs concurrently with the private-range kernel; the
+// caller's stream waits for it (event join) before the merge.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  std::mutex mu;
+};
+
+int side_stream(int device, SideStream** out) {
+  static std::mutex mu;
+  static SideStream* table[64] = {};
+  if (device < 0 || device >= 64) return set_err(KVP_EINVAL, "device %d", device);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!table[device]) {
+    auto* sd = new SideStream();  // lives until process exit
+    hipError_t e = hipStreamCreateWithFlags(&sd->s, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&sd->fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&sd->join, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      delete sd;
+      return hip_err(e, "side stream");
+    }
+    table[device] = sd;
+  }
+  *out = table[device];
+  return KVP_OK;
+}
+
 // Packs several arrays into one host buffer with 256-byte aligned offsets.
 struct Packer {
   std::vector<unsigned char> buf;
@@ -152,7 +181,8 @@ int upload_runs(const std::vector<kvp::PageRun>& runs, hipStream_t s, void** dev
 struct DecodeLayout {
   kvp::DecodePlan plan;
   Packer meta;
-  size_t off_wave = 0, off_group = 0, off_members = 0, off_part_base = 0, off_n_parts = 0, off_merge = 0;
+  size_t off_wave = 0, off_seg = 0, off_group = 0, off_members = 0, off_part_base = 0, off_n_parts = 0,
+         off_merge = 0;
   size_t off_acc = 0, off_ml = 0, total = 0;
 };
 
@@ -162,6 +192,7 @@ int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, con
   if (!st.ok()) return from_status(st);
   const auto& P = L->plan;
   L->off_wave = L->meta.add(P.wave_items.data(), P.wave_items.size() * sizeof(kvp::DecodeItem));
+  L->off_seg = L->meta.add(P.seg_off.data(), P.seg_off.size() * 4);
   L->off_group = L->meta.add(P.group_items.data(), P.group_items.size() * sizeof(kvp::DecodeItem));
   L->off_members = L->meta.add(P.members.data(), P.members.size() * 4);
   L->off_part_base = L->meta.add(P.part_base.data(), P.part_base.size() * 4);
@@ -439,15 +470,25 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   a.scale_log2 = scale * 1.4426950408889634f;
   a.err = pool->err;
   hipError_t e = hipSuccess;
+  kvp::DecodeArgs aw = a;
+  aw.items = reinterpret_cast<const kvp::DecodeItem*>(w + L.off_wave);
+  aw.seg_off = reinterpret_cast<const int32_t*>(w + L.off_seg);
+  aw.n_items = (int)P.seg_off.size() - 1;
   if (!P.group_items.empty()) {
+    SideStream* sd = nullptr;
+    rc = side_stream(pool->device, &sd);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> lock(sd->mu);
     a.items = reinterpret_cast<const kvp::DecodeItem*>(w + L.off_group);
     a.n_items = (int)P.group_items.size();
-    e = kvp::launch_decode_group(a, pool->head_dim, s);
-  }
-  if (e == hipSuccess && !P.wave_items.empty()) {
-    a.items = reinterpret_cast<const kvp::DecodeItem*>(w + L.off_wave);
-    a.n_items = (int)P.wave_items.size();
-    e = kvp::launch_decode_wave(a, pool->head_dim, s);
+    e = hipEventRecord(sd->fork, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(sd->s, sd->fork, 0);
+    if (e == hipSuccess) e = kvp::launch_decode_group(a, pool->head_dim, sd->s);
+    if (e == hipSuccess) e = hipEventRecord(sd->join, sd->s);
+    if (e == hipSuccess && aw.n_items > 0) e = kvp::launch_decode_wave(aw, pool->head_dim, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, sd->join, 0);
+  } else if (aw.n_items > 0) {
+    e = kvp::launch_decode_wave(aw, pool->head_dim, s);
   }
   if (e == hipSuccess && !P.merge_seqs.empty()) {
     kvp::MergeArgs m{};

@@ -23,6 +23,12 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
+// KV pages are read exactly once per call: stream them past the caches (nontemporal loads measure
+// ~7.0 TB/s on MI355X against ~6.2 TB/s for ordinary loads in a plain streaming-read test).
+__device__ __forceinline__ u32x4 ld16_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+
 __device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
                                                  c, 0, 0, 0);
@@ -143,16 +149,10 @@ __device__ __forceinline__ void write_state(const DecodeArgs& a, const DecodeIte
 // D/16 V loads of 16 bytes per lane (16 KB per wave at d = 128).
 // ---------------------------------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256) void decode_wave_kernel(DecodeArgs a) {
+__device__ __forceinline__ void decode_wave_chunk(const DecodeArgs& a, const DecodeItem& it, int kvh, int lane) {
   constexpr int NS = D / 32;
   constexpr int NT = D / 16;
   constexpr int KB = 16 * D;
-  const int lane = threadIdx.x & 63;
-  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int item = wid / a.Hkv;
-  const int kvh = wid - item * a.Hkv;
-  if (item >= a.n_items) return;
-  const DecodeItem it = a.items[item];
   const int q4 = lane >> 4, c16 = lane & 15;
   const int ncols = it.n_mem * a.G;
   const bool col_ok = c16 < ncols;
@@ -196,11 +196,11 @@ __global__ __launch_bounds__(256) void decode_wave_kernel(DecodeArgs a) {
     u32x4 kx[NS], ky[NS], vv[NT];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      kx[s] = ld16(kp + (4 * s + q4) * 128);
-      ky[s] = ld16(kp + (4 * s + q4) * 128 + 64);
+      kx[s] = ld16_stream(kp + (4 * s + q4) * 128);
+      ky[s] = ld16_stream(kp + (4 * s + q4) * 128 + 64);
     }
 #pragma unroll
-    for (int d = 0; d < NT; ++d) vv[d] = ld16(vp + d * 256);
+    for (int d = 0; d < NT; ++d) vv[d] = ld16_stream(vp + d * 256);
     f32x4 sx = {0.f, 0.f, 0.f, 0.f}, sy = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
@@ -215,8 +215,24 @@ __global__ __launch_bounds__(256) void decode_wave_kernel(DecodeArgs a) {
   if (bad && lane == 0) atomicCAS(a.err, 0, KVP_ERANGE);
   st.l += __shfl_xor(st.l, 16);
   st.l += __shfl_xor(st.l, 32);
-  if (!col_ok) return;
-  write_state<D, NT>(a, it, st, seq, head, q4);
+  if (col_ok) write_state<D, NT>(a, it, st, seq, head, q4);
+}
+
+// ---------------------------------------------------------------------------------------------------
+// Wave path: private page ranges, and shared-prefix ranges of groups with <= 16 query columns.  The
+// planner cuts the concatenated page ranges into equal segments; waves s*Hkv .. s*Hkv+Hkv-1 process
+// segment s, one KV head each, chunk after chunk.  Operands are loaded straight from HBM; each
+// two-page step issues 2*D/32 K loads and D/16 V loads of 16 bytes per lane (16 KB per wave, d = 128).
+// ---------------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void decode_wave_kernel(DecodeArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int seg = wid / a.Hkv;
+  const int kvh = wid - seg * a.Hkv;
+  if (seg >= a.n_items) return;
+  const int c1 = a.seg_off[seg + 1];
+  for (int c = a.seg_off[seg]; c < c1; ++c) decode_wave_chunk<D>(a, a.items[c], kvh, lane);
 }
 
 // ---------------------------------------------------------------------------------------------------
@@ -282,7 +298,7 @@ __global__ __launch_bounds__(256) void decode_group_kernel(DecodeArgs a) {
       const int pg = off / PB, inb = off - pg * PB;
       const bool ok = pg == 0 ? va : vb;
       const int id = pg == 0 ? ida : idb;
-      r[k] = ok ? ld16(reinterpret_cast<const unsigned char*>(hbase + (int64_t)id * page_stride) + inb)
+      r[k] = ok ? ld16_stream(reinterpret_cast<const unsigned char*>(hbase + (int64_t)id * page_stride) + inb)
                 : u32x4{0u, 0u, 0u, 0u};
     }
   };
@@ -385,11 +401,24 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
     const int h = kvh * G + hh;
     const float m = s_m[hh], inv = s_inv[hh];
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    if (inv > 0.0f)
-      for (int j = 0; j < P; ++j) {
-        const float w = fast_exp2(a.part_ml[(base + j) * a.Hq + h].x - m);
-        acc += w * *reinterpret_cast<const f32x4*>(a.part_acc + ((base + j) * a.Hq + h) * D + 4 * d4);
+    if (inv > 0.0f) {
+      const float2* ml = a.part_ml + base * a.Hq + h;
+      const float* pa = a.part_acc + (base * a.Hq + h) * D + 4 * d4;
+      const int64_t sa = (int64_t)a.Hq * D;
+      int j = 0;
+      for (; j + 4 <= P; j += 4) {  // four independent loads in flight, accumulated in partial order
+        f32x4 v[4];
+        float w[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          v[u] = *reinterpret_cast<const f32x4*>(pa + (j + u) * sa);
+          w[u] = ml[(int64_t)(j + u) * a.Hq].x;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc += fast_exp2(w[u] - m) * v[u];
       }
+      for (; j < P; ++j) acc += fast_exp2(ml[(int64_t)j * a.Hq].x - m) * *reinterpret_cast<const f32x4*>(pa + j * sa);
+    }
     acc *= inv;
     const int64_t oi = ((int64_t)seq * a.Hq + h) * D + 4 * d4;
     if (a.out_f32) {
@@ -406,7 +435,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
 }  // namespace
 
 hipError_t launch_decode_wave(const DecodeArgs& a, int D, hipStream_t s) {
-  const int64_t waves = (int64_t)a.n_items * a.Hkv;
+  const int64_t waves = (int64_t)a.n_items * a.Hkv;  // one wave per (segment, KV head)
   if (waves == 0) return hipSuccess;
   const dim3 grid((unsigned)((waves + 3) / 4));
   if (D == 128) hipLaunchKernelGGL(decode_wave_kernel<128>, grid, dim3(256), 0, s, a);

@@ -46,7 +46,8 @@ struct DecodeArgs {
   const int32_t* bt;
   int maxp;
   const DecodeItem* items;
-  int n_items;
+  int n_items;                // group kernel: items; wave kernel: segments
+  const int32_t* seg_off;     // wave kernel: [segments + 1] chunk offsets
   const int32_t* members;
   const int32_t* part_base;
   float* part_acc;          // [parts, Hq, D]

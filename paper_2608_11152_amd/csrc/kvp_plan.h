@@ -12,6 +12,8 @@ namespace kvp {
 constexpr int kPage = 16;
 constexpr int kMaxColsPerWave = 16;   // query columns one wave's MFMA tile holds (members x heads)
 constexpr int kMaxColsPerGroup = 64;  // query columns one shared-prefix workgroup holds (4 waves)
+constexpr int kMinSegmentPages = 32;  // smallest page count of a decode wave segment
+constexpr int kGroupChunkPages = 16;  // pages per workgroup of the LDS-staged shared-prefix kernel
 
 // One unit of decode work: one KV head of it is processed by one wave (private, <= 16 query columns)
 // or one 4-wave workgroup (shared prefix, <= 64 query columns).  Mirrors kvp_plan_decode's 8 ints.
@@ -28,14 +30,15 @@ struct DecodeItem {
 static_assert(sizeof(DecodeItem) == 32, "DecodeItem is uploaded as raw bytes");
 
 struct DecodePlan {
-  std::vector<DecodeItem> wave_items;   // private items and prefix items with n_mem * G <= 16
+  std::vector<DecodeItem> wave_items;   // chunks in segment order (private and <= 16-column prefix)
+  std::vector<int32_t> seg_off;         // [segments + 1]: chunks of segment s are seg_off[s]..seg_off[s+1]
   std::vector<DecodeItem> group_items;  // prefix items with 16 < n_mem * G <= 64 (LDS-staged kernel)
   std::vector<int32_t> members;         // member lists referenced by items
   std::vector<int32_t> part_base;       // [B] first partial index of each sequence
   std::vector<int32_t> n_parts;         // [B] partial count of each sequence
   std::vector<int32_t> merge_seqs;      // sequences whose output the merge kernel writes (0 or >= 2 parts)
   int32_t total_parts = 0;
-  int32_t pages_per_split = 0;
+  int32_t pages_per_split = 0;          // pages per wave segment
 };
 
 // Prefill: one 4-wave workgroup per (session, kv head, 128-row query tile).

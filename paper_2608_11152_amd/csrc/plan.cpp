@@ -50,21 +50,9 @@ static int64_t decode_target_waves() {
   static const int64_t v = [] {
     const char* e = std::getenv("KVP_DECODE_WAVES");
     const long x = e ? std::strtol(e, nullptr, 10) : 0;
-    return x > 0 ? (int64_t)x : (int64_t)4096;
+    return x > 0 ? (int64_t)x : (int64_t)2048;
   }();
   return v;
-}
-
-// Split [lo, hi) pages into nearly equal ranges of at most `ch` pages; interior boundaries are even so
-// that the kernels' two-page steps never straddle a boundary.
-static void split_range(int lo, int hi, int ch, std::vector<std::pair<int, int>>* out) {
-  out->clear();
-  const int n = hi - lo;
-  if (n <= 0) return;
-  const int parts = (n + ch - 1) / ch;
-  int len = (n + parts - 1) / parts;
-  len = (len + 1) & ~1;
-  for (int a = lo; a < hi; a += len) out->emplace_back(a, std::min(hi, a + len));
 }
 
 Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_prefix* gp, int Hq, int Hkv,
@@ -99,87 +87,126 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   for (int i = 0; i < B; ++i)
     if (seq_lens[i] > 0 && shared_of(i) > 0) mem[gp->group_id[i]].push_back(i);
 
-  // Pages per split: aim for about decode_target_waves() waves (several rounds of the ~12 waves per CU
-  // that fit on 256 CUs) so equal-sized splits balance across the chip; never below 32 pages (512 tokens),
-  // so a split's partial (G x d fp32 written, then read by the merge) stays within ~2% of its KV bytes.
-  int64_t page_heads = 0;
-  for (int i = 0; i < B; ++i) {
-    const int np = (seq_lens[i] + kPage - 1) / kPage;
-    page_heads += (int64_t)(np - (seq_lens[i] > 0 ? shared_of(i) : 0)) * Hkv;
-  }
-  for (int g = 0; g < NG; ++g)
-    if (!mem[g].empty()) page_heads += (int64_t)gp->shared_pages[g] * Hkv;
-  const int64_t waves = decode_target_waves();
-  int64_t ch = (page_heads + waves - 1) / waves;
-  ch = std::max<int64_t>(32, std::min<int64_t>(1024, ch));
-  ch = (ch + 1) & ~1;
-  plan->pages_per_split = (int)ch;
-
-  std::vector<int> n_prefix(B, 0), n_priv(B, 0);
-  std::vector<std::pair<int, int>> rng;
-  // Shared-prefix items: one per (subgroup, split).  A subgroup holds at most 64 query columns.
-  struct Pending { DecodeItem it; std::vector<int> mems; };
-  std::vector<Pending> prefix_items;
+  // Units: contiguous page ranges read for one set of query columns.  A group's shared prompt pages
+  // form one unit per subgroup (<= 64 query columns, so the pages are read once per subgroup); each
+  // sequence's pages after its shared prefix form one private unit.
+  struct Unit {
+    int kind, row, lo, hi, tok_end;
+    std::vector<int> mems;
+  };
+  std::vector<Unit> wave_units, group_units;
+  std::vector<int> group_unit_of(B, -1), wave_unit_of(B, -1);  // shared-prefix unit of each member
+  const int per_sub = std::max(1, kMaxColsPerGroup / G);
   for (int g = 0; g < NG; ++g) {
     if (mem[g].empty()) continue;
     const int S = gp->shared_pages[g];
-    split_range(0, S, (int)ch, &rng);
-    const int per_sub = std::max(1, kMaxColsPerGroup / G);
     for (size_t m0 = 0; m0 < mem[g].size(); m0 += per_sub) {
       const size_t m1 = std::min(mem[g].size(), m0 + per_sub);
-      for (size_t k = 0; k < rng.size(); ++k) {
-        Pending p;
-        p.it = DecodeItem{1, mem[g][m0], rng[k].first, rng[k].second, S * kPage, 0, (int)(m1 - m0), (int)k};
-        p.mems.assign(mem[g].begin() + m0, mem[g].begin() + m1);
-        prefix_items.push_back(std::move(p));
-      }
+      Unit u{1, mem[g][m0], 0, S, S * kPage, std::vector<int>(mem[g].begin() + m0, mem[g].begin() + m1)};
+      const bool wide = (int)u.mems.size() * G > kMaxColsPerWave;
+      for (int i : u.mems) (wide ? group_unit_of : wave_unit_of)[i] = (int)(wide ? group_units : wave_units).size();
+      (wide ? group_units : wave_units).push_back(std::move(u));
     }
-    for (int i : mem[g]) n_prefix[i] = (int)rng.size();
   }
-  // Private items: the pages after the shared prefix, split.
-  std::vector<DecodeItem> priv;
   for (int i = 0; i < B; ++i) {
     if (seq_lens[i] <= 0) continue;
     const int lo = shared_of(i);
     const int hi = (seq_lens[i] + kPage - 1) / kPage;
-    split_range(lo, hi, (int)ch, &rng);
-    n_priv[i] = (int)rng.size();
-    for (size_t k = 0; k < rng.size(); ++k)
-      priv.push_back(DecodeItem{0, i, rng[k].first, rng[k].second, seq_lens[i], i, 1, n_prefix[i] + (int)k});
+    if (hi > lo) wave_units.push_back(Unit{0, i, lo, hi, seq_lens[i], {i}});
   }
 
-  // Partial slots per sequence; a sequence with exactly one private split writes its output directly.
+  // Wave-path units are cut into equal segments of consecutive pages ("stream-K" over the concatenated
+  // unit list): segment s is processed by waves s*Hkv .. s*Hkv+Hkv-1 (one per KV head), so every wave
+  // streams the same number of pages whatever the length skew, and a sequence is split only where a
+  // segment boundary falls inside it.  About decode_target_waves() waves: one round of the waves that
+  // are resident at once on 256 CUs.  Segments hold at least 32 pages (512 tokens) so that a chunk's
+  // partial (G x d fp32 written, then read by the merge) stays within ~2% of its KV bytes.
+  int64_t total_pages = 0;
+  for (const Unit& u : wave_units) total_pages += u.hi - u.lo;
+  const int64_t segs_target = std::max<int64_t>(1, decode_target_waves() / Hkv);
+  int64_t seg_pages = (total_pages + segs_target - 1) / segs_target;
+  seg_pages = std::max<int64_t>(kMinSegmentPages, (seg_pages + 1) & ~int64_t(1));
+  plan->pages_per_split = (int)seg_pages;
+
+  struct Chunk { int unit, lo, hi; };
+  std::vector<Chunk> wave_chunks;
+  std::vector<int> seg_of_chunk;
+  std::vector<int> n_chunks_wave(wave_units.size(), 0);
+  {
+    int64_t fill = 0;
+    int seg = 0;
+    for (size_t u = 0; u < wave_units.size(); ++u) {
+      int lo = wave_units[u].lo;
+      while (lo < wave_units[u].hi) {
+        const int take = (int)std::min<int64_t>(wave_units[u].hi - lo, seg_pages - fill);
+        wave_chunks.push_back(Chunk{(int)u, lo, lo + take});
+        seg_of_chunk.push_back(seg);
+        n_chunks_wave[u]++;
+        lo += take;
+        fill += take;
+        if (fill == seg_pages) {
+          fill = 0;
+          ++seg;
+        }
+      }
+    }
+  }
+  // Wide shared-prefix units (LDS-staged workgroup kernel): fixed chunks of kGroupChunkPages pages.
+  std::vector<Chunk> group_chunks;
+  std::vector<int> n_chunks_group(group_units.size(), 0);
+  for (size_t u = 0; u < group_units.size(); ++u)
+    for (int lo = group_units[u].lo; lo < group_units[u].hi; lo += kGroupChunkPages) {
+      group_chunks.push_back(Chunk{(int)u, lo, std::min(group_units[u].hi, lo + kGroupChunkPages)});
+      n_chunks_group[u]++;
+    }
+
+  // Partial slots: per sequence, its shared-prefix chunks first (the same slot index for every member
+  // of a subgroup), then its private chunks.  A sequence with a single private chunk and no prefix
+  // writes its output directly (slot -1) and needs no merge.
+  std::vector<int> n_prefix(B, 0), n_priv(B, 0);
+  for (int i = 0; i < B; ++i) {
+    if (group_unit_of[i] >= 0) n_prefix[i] = n_chunks_group[group_unit_of[i]];
+    if (wave_unit_of[i] >= 0) n_prefix[i] = n_chunks_wave[wave_unit_of[i]];
+  }
+  for (size_t u = 0; u < wave_units.size(); ++u)
+    if (wave_units[u].kind == 0) n_priv[wave_units[u].row] = n_chunks_wave[u];
   plan->part_base.assign(B, 0);
   plan->n_parts.assign(B, 0);
   int32_t total = 0;
   for (int i = 0; i < B; ++i) {
     const int np = n_prefix[i] + n_priv[i];
-    const bool direct = (np == 1 && n_priv[i] == 1);
+    const bool direct = (n_prefix[i] == 0 && n_priv[i] == 1);
     plan->n_parts[i] = direct ? 1 : np;
     plan->part_base[i] = total;
-    if (!direct) total += np;
-    if (!direct) plan->merge_seqs.push_back(i);
+    if (!direct) {
+      total += np;
+      plan->merge_seqs.push_back(i);
+    }
   }
   plan->total_parts = total;
 
-  for (auto& p : prefix_items) {
-    p.it.mem_off = (int)plan->members.size();
-    plan->members.insert(plan->members.end(), p.mems.begin(), p.mems.end());
-    if (p.it.n_mem * G <= kMaxColsPerWave) plan->wave_items.push_back(p.it);
-    else plan->group_items.push_back(p.it);
-  }
-  for (auto it : priv) {
-    it.mem_off = (int)plan->members.size();
-    plan->members.push_back(it.row);
-    if (n_prefix[it.row] + n_priv[it.row] == 1) it.slot = -1;
-    plan->wave_items.push_back(it);
-  }
-  // Longest ranges first (stable, so the order stays a pure function of the inputs).
-  auto longer = [](const DecodeItem& a, const DecodeItem& b) {
-    return (a.page_hi - a.page_lo) > (b.page_hi - b.page_lo);
+  auto emit = [&](const Unit& un, const Chunk& c, int k) {
+    DecodeItem it{un.kind, un.row, c.lo, c.hi, un.tok_end, (int)plan->members.size(), (int)un.mems.size(), 0};
+    plan->members.insert(plan->members.end(), un.mems.begin(), un.mems.end());
+    if (un.kind == 1) it.slot = k;
+    else it.slot = (n_prefix[un.row] == 0 && n_priv[un.row] == 1) ? -1 : n_prefix[un.row] + k;
+    return it;
   };
-  std::stable_sort(plan->wave_items.begin(), plan->wave_items.end(), longer);
-  std::stable_sort(plan->group_items.begin(), plan->group_items.end(), longer);
+  {
+    std::vector<int> k_of(wave_units.size(), 0);
+    plan->seg_off.push_back(0);
+    for (size_t c = 0; c < wave_chunks.size(); ++c) {
+      if (c > 0 && seg_of_chunk[c] != seg_of_chunk[c - 1]) plan->seg_off.push_back((int)c);
+      const int u = wave_chunks[c].unit;
+      plan->wave_items.push_back(emit(wave_units[u], wave_chunks[c], k_of[u]++));
+    }
+    plan->seg_off.push_back((int)wave_chunks.size());
+    if (wave_chunks.empty()) plan->seg_off.assign(1, 0);
+  }
+  {
+    std::vector<int> k_of(group_units.size(), 0);
+    for (const Chunk& c : group_chunks) plan->group_items.push_back(emit(group_units[c.unit], c, k_of[c.unit]++));
+  }
   return {};
 }
 

@@ -45,7 +45,7 @@ def _coverage(seq_lens, gid=None, shared=None, Hq=32, Hkv=4):
     slots = [set() for _ in range(B)]
     direct = [0] * B
     for kind, row, lo, hi, tok_end, first, nmem, slot in items.tolist():
-        assert 0 < hi - lo <= ch
+        assert 0 < hi - lo <= max(ch, 16)
         if kind == 0:
             assert first == row and nmem == 1 and tok_end == seq_lens[row]
             cover[row][lo:hi] += 1
@@ -76,6 +76,22 @@ def test_plan_covers_every_page_once(name):
     w = W.make_workload(name)
     gid = w.group_id if w.num_groups else None
     _coverage(w.decode_len, gid, w.shared_pages if gid is not None else None, w.Hq, w.Hkv)
+
+
+def test_plan_segments_are_balanced():
+    """Wave-path chunks are cut into equal page segments whatever the length skew."""
+    w = W.make_workload("mixed")
+    gp = kp.group_prefix(w.group_id, w.shared_pages)
+    items, parts, seg = kp.kvp_plan_decode(w.decode_len, w.Hq, w.Hkv, gp)
+    wave = items[(items[:, 0] == 0) | (items[:, 6] * (w.Hq // w.Hkv) <= 16)]
+    pages = int((wave[:, 3] - wave[:, 2]).sum())
+    n_full = pages // seg
+    assert n_full >= 1 and parts < len(items) + w.B
+    # walking the chunks in order, the running page count crosses every multiple of seg exactly at a
+    # chunk boundary (segments are exactly seg pages, except the last)
+    run = np.cumsum(wave[:, 3] - wave[:, 2])
+    for k in range(1, n_full + 1):
+        assert k * seg in set(run.tolist())
 
 
 def test_plan_prefix_counted_once_per_group():
