@@ -80,48 +80,66 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   const int32_t* btr = a.bt + (int64_t)it.seq * a.maxp;
   bool bad = false;
 
-  // Stage `st` = logical pages 4*st .. 4*st+3.  Pages beyond the tile's keys, pages with invalid ids and
-  // token slots beyond n_keys in the last page are staged as zeros.
+  // Stage `st` = logical pages 4*st .. 4*st+3, staged through registers.  Page ids and their validity
+  // are uniform per page (scalar loads).  `fetch` only issues the loads (a missing or invalid page
+  // reads page 0), so they stay in flight while the current stage computes; `store` then zeroes what
+  // must not be used and writes LDS: pages outside the tile's key range or with invalid ids, and the
+  // slots past the end of the sequence in its last page (stale pool contents).
+  const int seq_tokens = ctx + C;
+  constexpr int CPP = NCH / NPG;  // 16-byte chunks per page per thread
+  auto page_ok = [&](int st, int pg, int* id_out) {
+    const int lp = st * NPG + pg;
+    const bool inr = lp < n_pages;
+    const int id = inr ? btr[lp] : 0;
+    const bool ok = inr && (unsigned)id < (unsigned)a.num_pages;
+    bad |= inr && !ok;
+    *id_out = ok ? id : 0;
+    return ok;
+  };
   auto fetch = [&](int st, u32x4 (&r)[NCH]) {
 #pragma unroll
-    for (int k = 0; k < NCH; ++k) {
-      const int off = (k * 256 + tid) * 16;
-      const int pg = off / PB, inb = off - pg * PB;
-      const int lp = st * NPG + pg;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (lp < n_pages) {
-        const int id = btr[lp];
-        if ((unsigned)id < (unsigned)a.num_pages) {
-          v = ld16(reinterpret_cast<const unsigned char*>(hbase + (int64_t)id * page_stride) + inb);
-          const int valid = n_keys - lp * 16;  // tokens of this page inside the tile's key range
-          if (valid < 16) {
-            if (inb < 2 * KB) {
-              if (((inb >> 4) & 15) >= valid) v = u32x4{0u, 0u, 0u, 0u};
-            } else {
-              const int h = ((inb - 2 * KB) >> 8) & 1;  // V chunk holds slots 8h..8h+7
+    for (int pg = 0; pg < NPG; ++pg) {
+      int id;
+      page_ok(st, pg, &id);
+      const unsigned char* src = reinterpret_cast<const unsigned char*>(hbase + (int64_t)id * page_stride) + tid * 16;
 #pragma unroll
-              for (int w = 0; w < 4; ++w) {
-                const unsigned lo = slot_token(8 * h + 2 * w) < valid ? 0xFFFFu : 0u;
-                const unsigned hi = slot_token(8 * h + 2 * w + 1) < valid ? 0xFFFF0000u : 0u;
-                v[w] &= lo | hi;
-              }
-            }
-          }
-        } else {
-          bad = true;
-        }
-      }
-      r[k] = v;
+      for (int c = 0; c < CPP; ++c) r[pg * CPP + c] = ld16(src + c * (256 * 16));
     }
   };
-  auto store = [&](int buf, const u32x4 (&r)[NCH]) {
+  auto store = [&](int st, int buf, u32x4 (&r)[NCH]) {
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      int id;
+      if (!page_ok(st, pg, &id))
+#pragma unroll
+        for (int c = 0; c < CPP; ++c) r[pg * CPP + c] = u32x4{0u, 0u, 0u, 0u};
+      const int valid = seq_tokens - (st * NPG + pg) * 16;  // tokens of this page inside the sequence
+      if (valid < 16) {
+#pragma unroll
+        for (int c = 0; c < CPP; ++c) {
+          const int inb = c * (256 * 16) + tid * 16;
+          u32x4& v = r[pg * CPP + c];
+          if (inb < 2 * KB) {
+            if (((inb >> 4) & 15) >= valid) v = u32x4{0u, 0u, 0u, 0u};
+          } else {
+            const int h = ((inb - 2 * KB) >> 8) & 1;  // V chunk holds slots 8h..8h+7
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              const unsigned lo = slot_token(8 * h + 2 * w) < valid ? 0xFFFFu : 0u;
+              const unsigned hi = slot_token(8 * h + 2 * w + 1) < valid ? 0xFFFF0000u : 0u;
+              v[w] &= lo | hi;
+            }
+          }
+        }
+      }
+    }
 #pragma unroll
     for (int k = 0; k < NCH; ++k) *reinterpret_cast<u32x4*>(lds + buf * SB + (k * 256 + tid) * 16) = r[k];
   };
 
   u32x4 r[NCH];
   fetch(0, r);
-  store(0, r);
+  store(0, 0, r);
   __syncthreads();
   int buf = 0;
   for (int st = 0; st < n_stages; ++st) {
@@ -184,7 +202,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
       for (int d = 0; d < NDT; ++d) acc[d] = mfma32(ld16(vp + d * 1024), pb[pg], acc[d]);
     }
-    if (more) store(buf ^ 1, r);
+    if (more) store(st + 1, buf ^ 1, r);
     __syncthreads();
     buf ^= 1;
   }
