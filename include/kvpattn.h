@@ -137,8 +137,10 @@ int paged_decode_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int nu
  *   group_prefix  host, nullable: members' shared prompt pages are read once per group
  *   out           device [num_seqs, num_q_heads, head_dim], out_dtype KVP_BF16 or KVP_F32
  *   ws            device workspace of ws_bytes >= paged_decode_workspace_size(...)
+ *   scale         softmax scale applied to q . k (finite, > 0; usually 1 / sqrt(head_dim))
  * Errors: KVP_ERANGE if seq_lens[i] > maxp * 16; KVP_EGROUP if a group id is out of range or a member's
- * seq_len is shorter than its group's shared pages; KVP_EWORKSPACE if ws_bytes is too small. */
+ * seq_len is shorter than its group's shared pages; KVP_EWORKSPACE if ws_bytes is too small; KVP_EINVAL
+ * if scale is not finite and positive. */
 int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
                       const int32_t* seq_lens, int num_seqs, const kvp_group_prefix* group_prefix,
                       int num_q_heads, float scale, void* out, int out_dtype, void* ws, size_t ws_bytes,
@@ -160,7 +162,9 @@ int prefix_chunk_prefill_workspace_size(kvp_pool_t pool, const int32_t* ctx_lens
  *   block_tables  device int32 [num_seqs, maxp] (row i = session i)
  *   ctx_lens      host int32 [num_seqs];  cu_q host int32 [num_seqs + 1]
  *   out           device [cu_q[num_seqs], num_q_heads, head_dim], out_dtype KVP_BF16 or KVP_F32
- * Errors: KVP_ERANGE if ctx_lens[i] + chunk > maxp * 16; KVP_EWORKSPACE if ws_bytes is too small. */
+ *   scale         softmax scale applied to q . k (finite, > 0)
+ * Errors: KVP_ERANGE if ctx_lens[i] + chunk > maxp * 16; KVP_EWORKSPACE if ws_bytes is too small;
+ * KVP_EINVAL if scale is not finite and positive. */
 int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables,
                               int maxp, const int32_t* ctx_lens, const int32_t* cu_q, int num_seqs,
                               int num_q_heads, float scale, void* out, int out_dtype, void* ws,

@@ -441,7 +441,7 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   if (num_seqs == 0) return KVP_OK;
   if (!q || !out || !block_tables || !seq_lens) return set_err(KVP_EINVAL, "NULL pointer argument");
   if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
-  if (!std::isfinite(scale)) return set_err(KVP_EINVAL, "scale is not finite");
+  if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
   DecodeLayout L;
   rc = layout_decode(pool, seq_lens, num_seqs, maxp, group_prefix, num_q_heads, &L);
   if (rc) return rc;
@@ -526,7 +526,7 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
   if (num_seqs == 0) return KVP_OK;
   if (!q || !out || !block_tables || !ctx_lens || !cu_q) return set_err(KVP_EINVAL, "NULL pointer argument");
   if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
-  if (!std::isfinite(scale)) return set_err(KVP_EINVAL, "scale is not finite");
+  if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
   PrefillLayout L;
   rc = layout_prefill(pool, ctx_lens, cu_q, num_seqs, maxp, num_q_heads, &L);
   if (rc) return rc;

@@ -3,8 +3,8 @@
 //
 // One 4-wave workgroup per (session, KV head, 128 flattened query rows).  Query rows are flattened as
 // position * G + head-in-group, so every K/V tile loaded serves all G query heads of its KV head.  Keys
-// stream through LDS in stages of 4 pages (64 keys), double-buffered through registers so the next
-// stage's HBM reads overlap this stage's MFMA work.  Wave w owns 32 query rows:
+// stream through LDS in stages of 4 pages (64 keys), double-buffered with direct global->LDS copies so
+// the next stage's reads overlap this stage's MFMA work.  Wave w owns 32 query rows:
 //   S^T (64 keys x 32 rows) = K Q^T      v_mfma_f32_32x32x16_bf16, 2 key tiles x D/16 k-steps
 //   O^T (D x 32 rows)      += V^T P^T    the score tile's registers are the P^T operand (per page)
 // Masking is applied only to stages that reach past the wave's first query position (the diagonal).
@@ -74,91 +74,118 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
   for (int d = 0; d < NDT; ++d) acc[d] = f32x16{};
   float m_run = -INFINITY, l_run = 0.0f;
+  const float cs = a.scale_log2;
 
   const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
   const uint16_t* hbase = a.layer + (int64_t)it.kvh * 2 * KB;
-  const int32_t* btr = a.bt + (int64_t)it.seq * a.maxp;
+  // The block table is read-only for the kernel's lifetime: read it through the constant address space
+  // so page ids are scalar loads (counted apart from the LDS copies, which the compiler must not wait on).
+  typedef const __attribute__((address_space(4))) int32_t* const_i32p;
+  const_i32p btr = (const_i32p)(a.bt + (int64_t)it.seq * a.maxp);
   bool bad = false;
 
-  // Stage `st` = logical pages 4*st .. 4*st+3, staged through registers.  Page ids and their validity
-  // are uniform per page (scalar loads).  `fetch` only issues the loads (a missing or invalid page
-  // reads page 0), so they stay in flight while the current stage computes; `store` then zeroes what
-  // must not be used and writes LDS: pages outside the tile's key range or with invalid ids, and the
-  // slots past the end of the sequence in its last page (stale pool contents).
   const int seq_tokens = ctx + C;
   constexpr int CPP = NCH / NPG;  // 16-byte chunks per page per thread
-  auto page_ok = [&](int st, int pg, int* id_out) {
-    const int lp = st * NPG + pg;
-    const bool inr = lp < n_pages;
-    const int id = inr ? btr[lp] : 0;
-    const bool ok = inr && (unsigned)id < (unsigned)a.num_pages;
-    bad |= inr && !ok;
-    *id_out = ok ? id : 0;
-    return ok;
-  };
-  auto fetch = [&](int st, u32x4 (&r)[NCH]) {
+  // Stage `st` = logical pages 4*st .. 4*st+3, copied global -> LDS by the load unit itself
+  // (global_load_lds_dwordx4: each wave instruction lands 64 x 16 B contiguously at its LDS base), so
+  // no registers hold the next stage while the current one computes.  Page ids: four independent
+  // scalar loads, index clamped into the tile's page range so each is in bounds.  A missing or invalid
+  // page is read from page 0 and `patch` zeroes it once the copies have landed, together with the slots
+  // past the end of the sequence in its last page (stale pool contents).
+  auto fetch = [&](int st, int buf, bool (&okp)[NPG]) {
+    int ids[NPG];
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) ids[pg] = btr[min(st * NPG + pg, n_pages - 1)];
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) {
-      int id;
-      page_ok(st, pg, &id);
+      const bool inr = st * NPG + pg < n_pages;
+      okp[pg] = inr && (unsigned)ids[pg] < (unsigned)a.num_pages;
+      bad |= inr && !okp[pg];
+      const int id = okp[pg] ? ids[pg] : 0;
       const unsigned char* src = reinterpret_cast<const unsigned char*>(hbase + (int64_t)id * page_stride) + tid * 16;
 #pragma unroll
-      for (int c = 0; c < CPP; ++c) r[pg * CPP + c] = ld16(src + c * (256 * 16));
-    }
-  };
-  auto store = [&](int st, int buf, u32x4 (&r)[NCH]) {
-#pragma unroll
-    for (int pg = 0; pg < NPG; ++pg) {
-      int id;
-      if (!page_ok(st, pg, &id))
-#pragma unroll
-        for (int c = 0; c < CPP; ++c) r[pg * CPP + c] = u32x4{0u, 0u, 0u, 0u};
-      const int valid = seq_tokens - (st * NPG + pg) * 16;  // tokens of this page inside the sequence
-      if (valid < 16) {
-#pragma unroll
-        for (int c = 0; c < CPP; ++c) {
-          const int inb = c * (256 * 16) + tid * 16;
-          u32x4& v = r[pg * CPP + c];
-          if (inb < 2 * KB) {
-            if (((inb >> 4) & 15) >= valid) v = u32x4{0u, 0u, 0u, 0u};
-          } else {
-            const int h = ((inb - 2 * KB) >> 8) & 1;  // V chunk holds slots 8h..8h+7
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-              const unsigned lo = slot_token(8 * h + 2 * w) < valid ? 0xFFFFu : 0u;
-              const unsigned hi = slot_token(8 * h + 2 * w + 1) < valid ? 0xFFFF0000u : 0u;
-              v[w] &= lo | hi;
-            }
-          }
-        }
+      for (int c = 0; c < CPP; ++c) {
+        const int k = pg * CPP + c;
+        __builtin_amdgcn_global_load_lds(src + c * (256 * 16),
+                                         (__attribute__((address_space(3))) void*)(lds + buf * SB + k * 4096 + wv * 1024),
+                                         16, 0, 0);
       }
     }
-#pragma unroll
-    for (int k = 0; k < NCH; ++k) *reinterpret_cast<u32x4*>(lds + buf * SB + (k * 256 + tid) * 16) = r[k];
   };
+  auto patch = [&](int st, int buf, const bool (&okp)[NPG]) {
+    bool any = (st + 1) * NPG * 16 > seq_tokens;
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) any |= !okp[pg];
+    if (!any) return;
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      const int valid = okp[pg] ? seq_tokens - (st * NPG + pg) * 16 : 0;  // usable tokens of this page
+      if (valid >= 16) continue;
+#pragma unroll
+      for (int c = 0; c < CPP; ++c) {
+        const int inb = c * (256 * 16) + tid * 16;
+        u32x4* lp = reinterpret_cast<u32x4*>(lds + buf * SB + ((pg * CPP + c) * 256 + tid) * 16);
+        u32x4 v = *lp;
+        if (inb < 2 * KB) {
+          if (((inb >> 4) & 15) >= valid) v = u32x4{0u, 0u, 0u, 0u};
+        } else {
+          const int h = ((inb - 2 * KB) >> 8) & 1;  // V chunk holds slots 8h..8h+7
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const unsigned lo = slot_token(8 * h + 2 * w) < valid ? 0xFFFFu : 0u;
+            const unsigned hi = slot_token(8 * h + 2 * w + 1) < valid ? 0xFFFF0000u : 0u;
+            v[w] &= lo | hi;
+          }
+        }
+        *lp = v;
+      }
+    }
+  };
+  // vmcnt(0): the stage's LDS copies have landed (expcnt / lgkmcnt left unconstrained).
+  auto wait_copies = [] { __builtin_amdgcn_s_waitcnt(0x0F70); };
 
-  u32x4 r[NCH];
-  fetch(0, r);
-  store(0, 0, r);
+  bool okp[NPG];
+  fetch(0, 0, okp);
+  wait_copies();
+  patch(0, 0, okp);
   __syncthreads();
   int buf = 0;
   for (int st = 0; st < n_stages; ++st) {
     const bool more = st + 1 < n_stages;
-    if (more) fetch(st + 1, r);
+    if (more) fetch(st + 1, buf ^ 1, okp);
     const unsigned char* sb = lds + buf * SB;
-    f32x16 S[2];
+    // K operand fragments for both 32-key tiles are read from LDS up front, then the two independent
+    // MFMA chains are interleaved; the V fragments are read next so their latency hides behind the
+    // softmax.  Scheduling barriers keep this order.
+    u32x4 kf[2][NS];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      S[kk] = f32x16{};
       const unsigned char* kp = sb + (2 * kk + (l32 >> 4)) * PB + (g * 16 + (l32 & 15)) * 16;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) S[kk] = mfma32(ld16(kp + s * 512), qt[s], S[kk]);
+      for (int s = 0; s < NS; ++s) kf[kk][s] = ld16(kp + s * 512);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16 S[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) S[kk] = mfma32(kf[kk][s], qt[s], S[kk]);
+    __builtin_amdgcn_sched_barrier(0);
+    u32x4 vf[NPG][NDT];
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      const unsigned char* vp = sb + pg * PB + 2 * KB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 512;
+#pragma unroll
+      for (int d = 0; d < NDT; ++d) vf[pg][d] = ld16(vp + d * 1024);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // Softmax on raw scores: with c = scale * log2(e) > 0 (the host rejects other scales),
+    // max(c*s) = c*max(s), so one FMA per score feeds exp2.
     float t[32];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) t[kk * 16 + i] = S[kk][i] * a.scale_log2;
+      for (int i = 0; i < 16; ++i) t[kk * 16 + i] = S[kk][i];
     const int kbase = st * 64;
     if (kbase + 63 > wave_min_pos) {
 #pragma unroll
@@ -169,10 +196,11 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
           if (key > qpos) t[kk * 16 + i] = -INFINITY;
         }
     }
-    float mx = t[0];
+    float mx = fmaxf(fmaxf(t[0], t[1]), t[2]);
 #pragma unroll
-    for (int i = 1; i < 32; ++i) mx = fmaxf(mx, t[i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    for (int i = 3; i < 31; i += 2) mx = fmaxf(fmaxf(mx, t[i]), t[i + 1]);
+    mx = fmaxf(mx, t[31]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * cs;
     const bool need = mx > m_run + 8.0f;
     if (__any(need)) {
       const float alpha = need ? fast_exp2(m_run - mx) : 1.0f;
@@ -188,7 +216,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       float p[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        p[j] = fast_exp2(t[(pg >> 1) * 16 + (pg & 1) * 8 + j] - mr);
+        p[j] = fast_exp2(__builtin_fmaf(t[(pg >> 1) * 16 + (pg & 1) * 8 + j], cs, -mr));
         l_run += p[j];
       }
       pb[pg][0] = pack_bf16(p[0], p[1]);
@@ -198,11 +226,13 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     }
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) {
-      const unsigned char* vp = sb + pg * PB + 2 * KB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 512;
 #pragma unroll
-      for (int d = 0; d < NDT; ++d) acc[d] = mfma32(ld16(vp + d * 1024), pb[pg], acc[d]);
+      for (int d = 0; d < NDT; ++d) acc[d] = mfma32(vf[pg][d], pb[pg], acc[d]);
     }
-    if (more) store(st + 1, buf ^ 1, r);
+    if (more) {
+      wait_copies();
+      patch(st + 1, buf ^ 1, okp);
+    }
     __syncthreads();
     buf ^= 1;
   }

@@ -219,7 +219,9 @@ def test_prefill_shapes(ctx, C, G):
     if C == 1:
         dec = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, [n], scale=0.09)
         torch.cuda.synchronize()
-        assert_close(dec, out.cpu().numpy().astype(np.float64), "decode == prefill of one row", 1e-5, 1e-6)
+        # same bf16 weights and weight sums; only fp32 summation order differs (a rare bf16 rounding flip of
+        # one weight moves an output by ~2^-9 of that weight's share)
+        assert_close(dec, out.cpu().numpy().astype(np.float64), "decode == prefill of one row", 2e-4, 1e-5)
 
 
 # ------------------------------------------------------------------------------------------------
