@@ -37,10 +37,7 @@ def _hipcc() -> str:
 def _compile(src: str, hipcc: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
     path = os.path.join(CSRC, src)
-    if src.endswith(".hip"):
-        cmd = [hipcc, "-x", "hip", *HIP_ONLY, *COMMON, "-c", path, "-o", obj]
-    else:
-        cmd = [hipcc, *COMMON, "-c", path, "-o", obj]
+    cmd = [hipcc, "-x", "hip", *HIP_ONLY, *COMMON, "-c", path, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     err = "\n".join(l for l in (r.stderr or "").splitlines() if noise not in l)

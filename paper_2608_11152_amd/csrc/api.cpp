@@ -45,15 +45,27 @@ int hip_err(hipError_t e, const char* what) {
   return set_err(KVP_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-// Ring of pinned host staging slots.  A slot is reused only after the copy that last read it has
-// completed (its event), so consecutive calls do not wait on each other's GPU work.
+// Ring of pinned host staging slots.  A slot is reused only after the GPU work that last read it has
+// completed (its event), so consecutive calls do not wait on each other's GPU work.  A slot is either
+// the source of one asynchronous copy (`upload`) or, for small per-call metadata, read by the kernels
+// directly over the bus (`lease` ... `release`), which saves the copy engine's latency.
 class Staging {
  public:
-  int upload(void* dst, const void* src, size_t n, hipStream_t s) {
-    if (n == 0) return KVP_OK;
+  struct Lease {
+    void* host = nullptr;
+    int slot = -1;
+  };
+
+  int lease(size_t n, Lease* out) {
     std::lock_guard<std::mutex> lock(mu_);
-    Slot& sl = slots_[next_];
-    next_ = (next_ + 1) % kSlots;
+    int idx = -1;
+    for (int k = 0; k < kSlots && idx < 0; ++k) {
+      const int c = (next_ + k) % kSlots;
+      if (!slots_[c].leased) idx = c;
+    }
+    if (idx < 0) return set_err(KVP_EINVAL, "more than %d concurrent calls hold metadata slots", kSlots);
+    next_ = (idx + 1) % kSlots;
+    Slot& sl = slots_[idx];
     if (sl.pending) {
       hipError_t e = hipEventSynchronize(sl.ev);
       if (e != hipSuccess) return hip_err(e, "hipEventSynchronize(staging)");
@@ -72,13 +84,37 @@ class Staging {
       if (e != hipSuccess) return set_err(KVP_ENOMEM, "hipHostMalloc(%zu): %s", cap, hipGetErrorString(e));
       sl.cap = cap;
     }
-    std::memcpy(sl.host, src, n);
-    hipError_t e = hipMemcpyAsync(dst, sl.host, n, hipMemcpyHostToDevice, s);
-    if (e != hipSuccess) return hip_err(e, "hipMemcpyAsync(metadata)");
-    e = hipEventRecord(sl.ev, s);
+    sl.leased = true;
+    out->host = sl.host;
+    out->slot = idx;
+    return KVP_OK;
+  }
+
+  // Marks the end of the GPU work that reads the slot (enqueued on s) and returns the slot to the ring.
+  // Without work to wait for (record = false) the slot is simply released.
+  int release(const Lease& l, hipStream_t s, bool record = true) {
+    std::lock_guard<std::mutex> lock(mu_);
+    Slot& sl = slots_[l.slot];
+    sl.leased = false;
+    if (!record) return KVP_OK;
+    hipError_t e = hipEventRecord(sl.ev, s);
     if (e != hipSuccess) return hip_err(e, "hipEventRecord");
     sl.pending = true;
     return KVP_OK;
+  }
+
+  int upload(void* dst, const void* src, size_t n, hipStream_t s) {
+    if (n == 0) return KVP_OK;
+    Lease l;
+    int rc = lease(n, &l);
+    if (rc) return rc;
+    std::memcpy(l.host, src, n);
+    hipError_t e = hipMemcpyAsync(dst, l.host, n, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) {
+      release(l, s, false);
+      return hip_err(e, "hipMemcpyAsync(metadata)");
+    }
+    return release(l, s);
   }
 
  private:
@@ -88,6 +124,7 @@ class Staging {
     size_t cap = 0;
     hipEvent_t ev = nullptr;
     bool pending = false;
+    bool leased = false;
   };
   std::mutex mu_;
   Slot slots_[kSlots];
@@ -177,7 +214,8 @@ int upload_runs(const std::vector<kvp::PageRun>& runs, hipStream_t s, void** dev
   return staging().upload(*dev, runs.data(), n, s);
 }
 
-// Decode workspace: [metadata][partial accumulators][partial (m, l)].
+// Decode: the work list lives in a pinned staging slot (read by the kernels directly); the caller's
+// workspace holds [partial accumulators][partial (m, l)].
 struct DecodeLayout {
   kvp::DecodePlan plan;
   Packer meta;
@@ -198,7 +236,7 @@ int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, con
   L->off_part_base = L->meta.add(P.part_base.data(), P.part_base.size() * 4);
   L->off_n_parts = L->meta.add(P.n_parts.data(), P.n_parts.size() * 4);
   L->off_merge = L->meta.add(P.merge_seqs.data(), P.merge_seqs.size() * 4);
-  L->off_acc = L->meta.size();
+  L->off_acc = 0;
   L->off_ml = L->off_acc + (((size_t)P.total_parts * Hq * pool->head_dim * 4 + 255) & ~size_t(255));
   L->total = L->off_ml + (((size_t)P.total_parts * Hq * 8 + 255) & ~size_t(255));
   return KVP_OK;
@@ -445,20 +483,26 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   DecodeLayout L;
   rc = layout_decode(pool, seq_lens, num_seqs, maxp, group_prefix, num_q_heads, &L);
   if (rc) return rc;
-  if (!ws || ws_bytes < L.total)
+  if (L.total > 0 && (!ws || ws_bytes < L.total))
     return set_err(KVP_EWORKSPACE, "workspace of %zu bytes, %zu needed", ws ? ws_bytes : (size_t)0, L.total);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   unsigned char* w = reinterpret_cast<unsigned char*>(ws);
-  rc = staging().upload(w, L.meta.buf.data(), L.meta.buf.size(), s);
+  // The work list is read by the kernels straight from a pinned staging slot (a few KB to a few
+  // hundred KB, read once per wave), so no copy sits between the caller's previous work and the
+  // decode kernels.  The slot is released after the last kernel that reads it.
+  Staging::Lease lease;
+  rc = staging().lease(L.meta.buf.size(), &lease);
   if (rc) return rc;
+  std::memcpy(lease.host, L.meta.buf.data(), L.meta.buf.size());
+  const unsigned char* m = reinterpret_cast<const unsigned char*>(lease.host);
   const auto& P = L.plan;
   kvp::DecodeArgs a{};
   a.q = reinterpret_cast<const uint16_t*>(q);
   a.layer = layer_ptr(pool, layer);
   a.bt = block_tables;
   a.maxp = maxp;
-  a.members = reinterpret_cast<const int32_t*>(w + L.off_members);
-  a.part_base = reinterpret_cast<const int32_t*>(w + L.off_part_base);
+  a.members = reinterpret_cast<const int32_t*>(m + L.off_members);
+  a.part_base = reinterpret_cast<const int32_t*>(m + L.off_part_base);
   a.part_acc = reinterpret_cast<float*>(w + L.off_acc);
   a.part_ml = reinterpret_cast<float2*>(w + L.off_ml);
   a.out = out;
@@ -471,15 +515,18 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   a.err = pool->err;
   hipError_t e = hipSuccess;
   kvp::DecodeArgs aw = a;
-  aw.items = reinterpret_cast<const kvp::DecodeItem*>(w + L.off_wave);
-  aw.seg_off = reinterpret_cast<const int32_t*>(w + L.off_seg);
+  aw.items = reinterpret_cast<const kvp::DecodeItem*>(m + L.off_wave);
+  aw.seg_off = reinterpret_cast<const int32_t*>(m + L.off_seg);
   aw.n_items = (int)P.seg_off.size() - 1;
   if (!P.group_items.empty()) {
     SideStream* sd = nullptr;
     rc = side_stream(pool->device, &sd);
-    if (rc) return rc;
+    if (rc) {
+      staging().release(lease, s, false);
+      return rc;
+    }
     std::lock_guard<std::mutex> lock(sd->mu);
-    a.items = reinterpret_cast<const kvp::DecodeItem*>(w + L.off_group);
+    a.items = reinterpret_cast<const kvp::DecodeItem*>(m + L.off_group);
     a.n_items = (int)P.group_items.size();
     e = hipEventRecord(sd->fork, s);
     if (e == hipSuccess) e = hipStreamWaitEvent(sd->s, sd->fork, 0);
@@ -491,20 +538,22 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
     e = kvp::launch_decode_wave(aw, pool->head_dim, s);
   }
   if (e == hipSuccess && !P.merge_seqs.empty()) {
-    kvp::MergeArgs m{};
-    m.merge_seqs = reinterpret_cast<const int32_t*>(w + L.off_merge);
-    m.n_merge = (int)P.merge_seqs.size();
-    m.part_base = a.part_base;
-    m.n_parts = reinterpret_cast<const int32_t*>(w + L.off_n_parts);
-    m.part_acc = a.part_acc;
-    m.part_ml = a.part_ml;
-    m.out = out;
-    m.out_f32 = a.out_f32;
-    m.Hq = num_q_heads;
-    m.Hkv = pool->num_kv_heads;
-    e = kvp::launch_decode_merge(m, pool->head_dim, s);
+    kvp::MergeArgs mg{};
+    mg.merge_seqs = reinterpret_cast<const int32_t*>(m + L.off_merge);
+    mg.n_merge = (int)P.merge_seqs.size();
+    mg.part_base = a.part_base;
+    mg.n_parts = reinterpret_cast<const int32_t*>(m + L.off_n_parts);
+    mg.part_acc = a.part_acc;
+    mg.part_ml = a.part_ml;
+    mg.out = out;
+    mg.out_f32 = a.out_f32;
+    mg.Hq = num_q_heads;
+    mg.Hkv = pool->num_kv_heads;
+    e = kvp::launch_decode_merge(mg, pool->head_dim, s);
   }
-  return e == hipSuccess ? KVP_OK : hip_err(e, "paged_decode_attn launch");
+  const int rr = staging().release(lease, s, e == hipSuccess);
+  if (e != hipSuccess) return hip_err(e, "paged_decode_attn launch");
+  return rr;
 }
 
 int prefix_chunk_prefill_workspace_size(kvp_pool_t pool, const int32_t* ctx_lens, const int32_t* cu_q, int num_seqs,

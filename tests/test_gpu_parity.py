@@ -274,10 +274,21 @@ def test_host_errors_enqueue_nothing(cases):
     with pytest.raises(kp.KvpError) as e:
         kp.paged_decode_attn(q, c.pool, 0, c.bt, too_long, out=sentinel)
     assert e.value.code == kp.KVP_ERANGE
-    ws = torch.empty(8, dtype=torch.uint8, device="cuda")
+    # a workload with partials needs workspace; the tiny one (one split per sequence) needs none
+    assert kp.paged_decode_workspace_size(c.pool, w.decode_len, w.Hq) == 0
+    cr = get_case(cases, "rlvr_s")
+    need = kp.paged_decode_workspace_size(cr.pool, cr.w.decode_len, cr.w.Hq, cr.gp)
+    assert need > 8
+    ws = torch.empty(need - 8, dtype=torch.uint8, device="cuda")
+    sentinel_r = torch.full((cr.w.B, cr.w.Hq, cr.w.d), 7.0, device="cuda")
     with pytest.raises(kp.KvpError) as e:
-        kp.paged_decode_attn(q, c.pool, 0, c.bt, w.decode_len, out=sentinel, ws=ws)
+        kp.paged_decode_attn(to_dev_bits(cr.vals.q), cr.pool, 0, cr.bt, cr.w.decode_len, group_prefix=cr.gp,
+                             out=sentinel_r, ws=ws)
     assert e.value.code == kp.KVP_EWORKSPACE
+    assert torch.all(sentinel_r == 7.0)
+    with pytest.raises(kp.KvpError) as e:
+        kp.paged_decode_attn(q, c.pool, 0, c.bt, w.decode_len, out=sentinel, scale=-1.0)
+    assert e.value.code == kp.KVP_EINVAL
     with pytest.raises(kp.KvpError) as e:
         kp.paged_decode_attn(q, c.pool, 3, c.bt, w.decode_len, out=sentinel)
     assert e.value.code == kp.KVP_EINVAL
