@@ -136,35 +136,6 @@ Staging& staging() {
   return *s;
 }
 
-// A library-owned side stream per device (default priority) onto which paged_decode_attn forks the
-// LDS-staged shared-prefix kernel so that it runs concurrently with the private-range kernel; the
-// caller's stream waits for it (event join) before the merge.
-struct SideStream {
-  hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
-  std::mutex mu;
-};
-
-int side_stream(int device, SideStream** out) {
-  static std::mutex mu;
-  static SideStream* table[64] = {};
-  if (device < 0 || device >= 64) return set_err(KVP_EINVAL, "device %d", device);
-  std::lock_guard<std::mutex> lock(mu);
-  if (!table[device]) {
-    auto* sd = new SideStream();  // lives until process exit
-    hipError_t e = hipStreamCreateWithFlags(&sd->s, hipStreamNonBlocking);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&sd->fork, hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&sd->join, hipEventDisableTiming);
-    if (e != hipSuccess) {
-      delete sd;
-      return hip_err(e, "side stream");
-    }
-    table[device] = sd;
-  }
-  *out = table[device];
-  return KVP_OK;
-}
-
 // Packs several arrays into one host buffer with 256-byte aligned offsets.
 struct Packer {
   std::vector<unsigned char> buf;
@@ -513,30 +484,14 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   a.num_pages = pool->num_pages;
   a.scale_log2 = scale * 1.4426950408889634f;
   a.err = pool->err;
-  hipError_t e = hipSuccess;
-  kvp::DecodeArgs aw = a;
-  aw.items = reinterpret_cast<const kvp::DecodeItem*>(m + L.off_wave);
-  aw.seg_off = reinterpret_cast<const int32_t*>(m + L.off_seg);
-  aw.n_items = (int)P.seg_off.size() - 1;
-  if (!P.group_items.empty()) {
-    SideStream* sd = nullptr;
-    rc = side_stream(pool->device, &sd);
-    if (rc) {
-      staging().release(lease, s, false);
-      return rc;
-    }
-    std::lock_guard<std::mutex> lock(sd->mu);
-    a.items = reinterpret_cast<const kvp::DecodeItem*>(m + L.off_group);
-    a.n_items = (int)P.group_items.size();
-    e = hipEventRecord(sd->fork, s);
-    if (e == hipSuccess) e = hipStreamWaitEvent(sd->s, sd->fork, 0);
-    if (e == hipSuccess) e = kvp::launch_decode_group(a, pool->head_dim, sd->s);
-    if (e == hipSuccess) e = hipEventRecord(sd->join, sd->s);
-    if (e == hipSuccess && aw.n_items > 0) e = kvp::launch_decode_wave(aw, pool->head_dim, s);
-    if (e == hipSuccess) e = hipStreamWaitEvent(s, sd->join, 0);
-  } else if (aw.n_items > 0) {
-    e = kvp::launch_decode_wave(aw, pool->head_dim, s);
-  }
+  a.items = reinterpret_cast<const kvp::DecodeItem*>(m + L.off_wave);
+  a.seg_off = reinterpret_cast<const int32_t*>(m + L.off_seg);
+  a.n_items = (int)P.seg_off.size() - 1;
+  a.group_items = reinterpret_cast<const kvp::DecodeItem*>(m + L.off_group);
+  a.n_group_items = (int)P.group_items.size();
+  a.n_group_blocks = a.n_group_items * a.Hkv;
+  a.n_wave_blocks = (a.n_items * a.Hkv + 3) / 4;
+  hipError_t e = kvp::launch_decode(a, pool->head_dim, s);
   if (e == hipSuccess && !P.merge_seqs.empty()) {
     kvp::MergeArgs mg{};
     mg.merge_seqs = reinterpret_cast<const int32_t*>(m + L.off_merge);

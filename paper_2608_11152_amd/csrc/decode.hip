@@ -225,9 +225,9 @@ __device__ __forceinline__ void decode_wave_chunk(const DecodeArgs& a, const Dec
 // two-page step issues 2*D/32 K loads and D/16 V loads of 16 bytes per lane (16 KB per wave, d = 128).
 // ---------------------------------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256) void decode_wave_kernel(DecodeArgs a) {
+__device__ __forceinline__ void decode_wave_block(const DecodeArgs& a, int block) {
   const int lane = threadIdx.x & 63;
-  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wid = block * 4 + (threadIdx.x >> 6);
   const int seg = wid / a.Hkv;
   const int kvh = wid - seg * a.Hkv;
   if (seg >= a.n_items) return;
@@ -242,20 +242,28 @@ __global__ __launch_bounds__(256) void decode_wave_kernel(DecodeArgs a) {
 // columns 16w..16w+15 from LDS.  The prefix pages therefore cross HBM once per group.
 // ---------------------------------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256) void decode_group_kernel(DecodeArgs a) {
+struct GroupLds {
+  static constexpr int KB = 16 * D;      // elements per K (or V) block
+  static constexpr int PB = 4 * KB;      // bytes per (page, head): K + V blocks
+  static constexpr int PAD = 128;        // keeps the two staged pages on different LDS banks
+  static constexpr int SB = 2 * PB + PAD;
+  static constexpr int bytes = 2 * SB;   // double-buffered two-page stage
+};
+
+template <int D>
+__device__ __forceinline__ void decode_group_block(const DecodeArgs& a, int block, unsigned char* lds) {
   constexpr int NS = D / 32;
   constexpr int NT = D / 16;
-  constexpr int KB = 16 * D;           // elements per K (or V) block
-  constexpr int PB = 4 * KB;           // bytes per (page, head): K + V blocks
-  constexpr int PAD = 128;             // keeps the two staged pages on different LDS banks
-  constexpr int SB = 2 * PB + PAD;
+  constexpr int KB = GroupLds<D>::KB;
+  constexpr int PB = GroupLds<D>::PB;
+  constexpr int PAD = GroupLds<D>::PAD;
+  constexpr int SB = GroupLds<D>::SB;
   constexpr int NCH = 2 * PB / (256 * 16);
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2 * SB];
 
-  const int item = blockIdx.x / a.Hkv;
-  const int kvh = blockIdx.x - item * a.Hkv;
-  if (item >= a.n_items) return;
-  const DecodeItem it = a.items[item];
+  const int item = block / a.Hkv;
+  const int kvh = block - item * a.Hkv;
+  if (item >= a.n_group_items) return;
+  const DecodeItem it = a.group_items[item];
   const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, q4 = lane >> 4, c16 = lane & 15;
   const int ncols = it.n_mem * a.G;
   const int col = wv * 16 + c16;
@@ -358,6 +366,20 @@ __global__ __launch_bounds__(256) void decode_group_kernel(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------------------
+// One launch for both paths: blocks [0, n_wave_blocks) run 4 wave-path waves each; the remaining
+// blocks run the LDS-staged shared-prefix path, one per (prefix item, KV head).  Blocks are dispatched
+// in index order, so the wave blocks take the first round and the shared-prefix blocks run in the
+// slots the planner left free for them.  The two paths need the same number of registers to within a
+// few, so sharing a launch costs no occupancy and saves a launch boundary.
+// ---------------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[GroupLds<D>::bytes];
+  if ((int)blockIdx.x < a.n_wave_blocks) decode_wave_block<D>(a, blockIdx.x);
+  else decode_group_block<D>(a, (int)blockIdx.x - a.n_wave_blocks, lds);
+}
+
+// ---------------------------------------------------------------------------------------------------
 // Log-sum-exp merge: out = sum_j acc_j 2^(m_j - m) / sum_j l_j 2^(m_j - m), m = max_j m_j, in partial
 // order (fixed, so results are deterministic).  Empty partials (m = -inf, l = 0) carry zero weight; a
 // sequence with no partial gets a zero output.  One workgroup per (sequence, KV head): the G heads' max
@@ -434,20 +456,11 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
 
 }  // namespace
 
-hipError_t launch_decode_wave(const DecodeArgs& a, int D, hipStream_t s) {
-  const int64_t waves = (int64_t)a.n_items * a.Hkv;  // one wave per (segment, KV head)
-  if (waves == 0) return hipSuccess;
-  const dim3 grid((unsigned)((waves + 3) / 4));
-  if (D == 128) hipLaunchKernelGGL(decode_wave_kernel<128>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(decode_wave_kernel<64>, grid, dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_decode_group(const DecodeArgs& a, int D, hipStream_t s) {
-  const int64_t blocks = (int64_t)a.n_items * a.Hkv;
+hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.n_wave_blocks + a.n_group_blocks;
   if (blocks == 0) return hipSuccess;
-  if (D == 128) hipLaunchKernelGGL(decode_group_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(decode_group_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  if (D == 128) hipLaunchKernelGGL(decode_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(decode_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

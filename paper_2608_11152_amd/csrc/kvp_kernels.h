@@ -45,9 +45,13 @@ struct DecodeArgs {
   const uint16_t* layer;
   const int32_t* bt;
   int maxp;
-  const DecodeItem* items;
-  int n_items;                // group kernel: items; wave kernel: segments
-  const int32_t* seg_off;     // wave kernel: [segments + 1] chunk offsets
+  const DecodeItem* items;    // wave path: chunks in segment order
+  int n_items;                // wave path: segment count
+  const int32_t* seg_off;     // wave path: [segments + 1] chunk offsets
+  const DecodeItem* group_items;  // shared-prefix path (LDS-staged, > 16 query columns)
+  int n_group_items;
+  int n_group_blocks;         // n_group_items * Hkv
+  int n_wave_blocks;          // ceil(segments * Hkv / 4): one wave per (segment, KV head)
   const int32_t* members;
   const int32_t* part_base;
   float* part_acc;          // [parts, Hq, D]
@@ -90,8 +94,7 @@ struct PrefillArgs {
 hipError_t launch_append(const AppendArgs& a, int D, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, int D, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
-hipError_t launch_decode_wave(const DecodeArgs& a, int D, hipStream_t s);
-hipError_t launch_decode_group(const DecodeArgs& a, int D, hipStream_t s);
+hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s);
 hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s);
 hipError_t launch_prefill(const PrefillArgs& a, int D, hipStream_t s);
 

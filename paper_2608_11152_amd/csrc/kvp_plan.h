@@ -39,6 +39,7 @@ struct DecodePlan {
   std::vector<int32_t> merge_seqs;      // sequences whose output the merge kernel writes (0 or >= 2 parts)
   int32_t total_parts = 0;
   int32_t pages_per_split = 0;          // pages per wave segment
+  int32_t group_reserved_blocks = 0;    // block slots the wave budget leaves to the shared-prefix path
 };
 
 // Prefill: one 4-wave workgroup per (session, kv head, 128-row query tile).

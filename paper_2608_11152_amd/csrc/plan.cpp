@@ -2,6 +2,7 @@
 // Deterministic: a plan depends only on lengths, group structure and head counts, never on physical
 // page ids, so GPU results are bitwise reproducible under any page permutation.
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <numeric>
@@ -121,9 +122,22 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   // segment boundary falls inside it.  About decode_target_waves() waves: one round of the waves that
   // are resident at once on 256 CUs.  Segments hold at least 32 pages (512 tokens) so that a chunk's
   // partial (G x d fp32 written, then read by the merge) stays within ~2% of its KV bytes.
-  int64_t total_pages = 0;
+  int64_t total_pages = 0, group_pages = 0;
   for (const Unit& u : wave_units) total_pages += u.hi - u.lo;
-  const int64_t segs_target = std::max<int64_t>(1, decode_target_waves() / Hkv);
+  for (const Unit& u : group_units) group_pages += u.hi - u.lo;
+  // The LDS-staged shared-prefix blocks run in the same launch, after the wave blocks in grid order.
+  // Reserve block slots for them out of the one-round budget (4 waves per block), in proportion to
+  // their share of the pages weighted by their lower per-block throughput (about 2.5x less than four
+  // independent streaming waves), so they drain while the wave segments run instead of after them.
+  const int64_t budget_blocks = std::max<int64_t>(1, decode_target_waves() / 4);
+  int64_t reserve = 0;
+  if (group_pages > 0) {
+    const double wg = 2.5 * (double)group_pages, ww = (double)total_pages;
+    reserve = (int64_t)std::ceil((double)budget_blocks * wg / (wg + ww));
+    reserve = std::max<int64_t>(1, std::min<int64_t>(reserve, budget_blocks / 2));
+  }
+  plan->group_reserved_blocks = (int)reserve;
+  const int64_t segs_target = std::max<int64_t>(1, (budget_blocks - reserve) * 4 / Hkv);
   int64_t seg_pages = (total_pages + segs_target - 1) / segs_target;
   seg_pages = std::max<int64_t>(kMinSegmentPages, (seg_pages + 1) & ~int64_t(1));
   plan->pages_per_split = (int)seg_pages;
