@@ -79,6 +79,34 @@ def prefill_algorithmic_bytes(w) -> int:
     return toks * w.Hkv * w.d * 4 + int(w.prefill_chunk.sum()) * w.Hq * w.d * 4
 
 
+PROFILE_OF = {"mixed": "decode_prefill_mixed_step.md", "rlvr": "decode_rlvr_64x8.md",
+              "agentic": "decode_prefill_agentic_32x128k.md"}
+KERNEL_SOURCES = ("decode.hip", "prefill.hip", "plan.cpp", "kvp_layout.h", "kvp_kernels.h", "kvp_plan.h")
+
+
+def profiled_traffic(workload: str):
+    """Per-launch HBM bytes (FETCH_SIZE x2 + WRITE_SIZE, see the profile summary) for this workload, or
+    (None, None) when no summary exists or the kernel sources changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", PROFILE_OF.get(workload, "-"))
+    if not os.path.exists(path):
+        return None, None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.split(":")[0].strip() in ("kernel-source-sha256", "traffic-decode-bytes",
+                                                           "traffic-prefill-bytes"):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2608_11152_amd", "csrc", f), "rb").read())
+    if fields.get("kernel-source-sha256") != h.hexdigest():
+        return None, None
+    dec = fields.get("traffic-decode-bytes")
+    pf = fields.get("traffic-prefill-bytes")
+    return (int(float(dec)) if dec else None), (int(float(pf)) if pf else None)
+
+
 def cpu_baseline(w, vals, budget_s: float):
     """Time the CPU fp64 oracle (as it stands) on a bounded sample of the same decode workload."""
     import oracle
@@ -209,6 +237,7 @@ def main():
     copy_gbs = 5 * 2 * (1 << 30) / (c0.elapsed_time(c1) / 1e3) / 1e9
     del src, dst
 
+    traffic_dec, traffic_pf = profiled_traffic(args.workload)
     dec_bytes = decode_algorithmic_bytes(w)
     dec_s = float(np.mean(t_dec)) / 1e3
     dec_gbs = dec_bytes / dec_s / 1e9
@@ -237,7 +266,7 @@ def main():
         "append_ms": round(float(np.mean(t_app)), 4),
         "hbm_copy_gbs": round(copy_gbs, 1),
         "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic_dec,
                      "kernel": "paged_decode_attn (shared-prefix + split-KV partial kernels and LSE merge)",
                      "algorithmic_bytes_per_launch": dec_bytes},
     }
@@ -249,7 +278,8 @@ def main():
         res["prefill_tflops"] = round(flops / pf_s / 1e12, 2)
         res["roofline_prefill"] = {"bound": "mfma", "achieved": round(flops / pf_s / 1e12, 2),
                                    "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                                   "frac": round(flops / pf_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                                   "frac": round(flops / pf_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                                   "traffic": traffic_pf,
                                    "kernel": "prefix_chunk_prefill_attn", "algorithmic_flops_per_launch": flops,
                                    "algorithmic_bytes_per_launch": prefill_algorithmic_bytes(w)}
     if not args.no_cpu_baseline:
