@@ -342,3 +342,57 @@ def test_pool_reset_zeroes(cases):
     c.pool.reset()
     torch.cuda.synchronize()
     assert bool(torch.all(c.pool.layer_raw(0) == 0))
+
+
+@pytest.mark.parametrize("G,members,d", [(8, 3, 128), (16, 2, 128), (4, 12, 64), (8, 12, 128), (1, 80, 64),
+                                         (2, 5, 128), (16, 5, 64)])
+def test_decode_group_shapes(G, members, d):
+    """Shared-prefix groups of every tiling: 2 and 3 column tiles on the LDS path, subgroups (> 64
+    columns, with a remainder small enough for the wave path), G = 1 and G = 16, odd member counts."""
+    import torch
+    Hkv = 2
+    Hq = G * Hkv
+    rng = np.random.default_rng(G * 100 + members + d)
+    P = int(rng.integers(40, 300))           # prompt tokens; shared whole pages = P // 16
+    S = P // 16
+    priv = rng.integers(1, 500, size=members)
+    lens = (P + priv).astype(np.int32)
+    pages = [(int(n) + 15) // 16 for n in lens]
+    num_pages = S + sum(p - S for p in pages) + 7
+    perm = rng.permutation(num_pages).astype(np.int32)
+    maxp = max(pages)
+    bt = np.full((members, maxp), -1, np.int32)
+    nxt = S
+    for i in range(members):
+        bt[i, :S] = perm[:S]
+        k = pages[i] - S
+        bt[i, S:S + k] = perm[nxt:nxt + k]
+        nxt += k
+    prompt = W.f32_to_bf16_bits(rng.standard_normal((P, 2, Hkv, d), dtype=np.float32))
+    own = [W.f32_to_bf16_bits(rng.standard_normal((int(priv[i]), 2, Hkv, d), dtype=np.float32))
+           for i in range(members)]
+    qb = W.f32_to_bf16_bits(rng.standard_normal((members, Hq, d), dtype=np.float32))
+    pool = kp.Pool(1, num_pages, Hkv, d)
+    btd = torch.from_numpy(bt).cuda()
+    note(f"group shapes G={G} members={members} d={d} P={P}")
+    # the first member writes the shared prompt pages, then every member writes its tail + private tokens
+    cnt0 = np.zeros(members, np.int64)
+    cnt0[0] = S * 16
+    kv0 = to_dev_bits(prompt[:S * 16])
+    kp.kv_append(pool, 0, kv0[:, 0].contiguous(), kv0[:, 1].contiguous(), btd, np.zeros(members, np.int32),
+                 np.concatenate([[0], np.cumsum(cnt0)]).astype(np.int32))
+    rest = [np.concatenate([prompt[S * 16:], own[i]]) for i in range(members)]
+    kv1 = to_dev_bits(np.concatenate(rest))
+    cu1 = np.concatenate([[0], np.cumsum([len(r) for r in rest])]).astype(np.int32)
+    gp = kp.group_prefix(np.zeros(members, np.int32), np.array([S], np.int32))
+    kp.kv_append(pool, 0, kv1[:, 0].contiguous(), kv1[:, 1].contiguous(), btd, np.full(members, S * 16, np.int32),
+                 cu1, group_prefix=gp)
+    out = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, lens, group_prefix=gp, scale=0.11)
+    out_ng = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, lens, scale=0.11)
+    torch.cuda.synchronize()
+    assert pool.device_error() == kp.KVP_OK
+    ref = np.stack([oracle.decode_seq(qb[i], oracle.widen_bf16(np.concatenate([prompt, own[i]])[:, 0]),
+                                      oracle.widen_bf16(np.concatenate([prompt, own[i]])[:, 1]), 0.11)
+                    for i in range(members)])
+    assert_close(out, ref, f"group G={G} x{members} d={d}")
+    assert_close(out_ng, ref, f"ungrouped G={G} x{members} d={d}")
