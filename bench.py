@@ -107,6 +107,29 @@ def profiled_traffic(workload: str):
     return (int(float(dec)) if dec else None), (int(float(pf)) if pf else None)
 
 
+def library_gemm_tflops(dev, stream, n: int = 8192, reps: int = 10) -> float:
+    """bf16 dense GEMM rate of the vendor library (torch.matmul -> hipBLASLt) on N(0,1) operands.
+
+    The chip's clock under dense bf16 matrix load depends on the operand data (random operands draw more
+    power than constants), so this is the practical MFMA ceiling next to which the prefill rate is read.
+    """
+    import torch
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    a = torch.randn(n, n, generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    b = torch.randn(n, n, generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    for _ in range(3):
+        c = a @ b
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        c = a @ b
+    e1.record(stream)
+    torch.cuda.synchronize()
+    del a, b, c
+    return round(2.0 * n ** 3 * reps / (e0.elapsed_time(e1) / 1e3) / 1e12, 1)
+
+
 def cpu_baseline(w, vals, budget_s: float):
     """Time the CPU fp64 oracle (as it stands) on a bounded sample of the same decode workload."""
     import oracle
@@ -236,6 +259,7 @@ def main():
     torch.cuda.synchronize()
     copy_gbs = 5 * 2 * (1 << 30) / (c0.elapsed_time(c1) / 1e3) / 1e9
     del src, dst
+    gemm_tflops = library_gemm_tflops(dev, stream) if has_prefill else None
 
     traffic_dec, traffic_pf = profiled_traffic(args.workload)
     dec_bytes = decode_algorithmic_bytes(w)
@@ -281,7 +305,9 @@ def main():
                                    "frac": round(flops / pf_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
                                    "traffic": traffic_pf,
                                    "kernel": "prefix_chunk_prefill_attn", "algorithmic_flops_per_launch": flops,
-                                   "algorithmic_bytes_per_launch": prefill_algorithmic_bytes(w)}
+                                   "algorithmic_bytes_per_launch": prefill_algorithmic_bytes(w),
+                                   "library_gemm_tflops": gemm_tflops,
+                                   "frac_of_library_gemm": round(flops / pf_s / 1e12 / gemm_tflops, 4)}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, vals, args.cpu_seconds)
     print(json.dumps(res), flush=True)
