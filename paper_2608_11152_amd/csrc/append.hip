@@ -11,6 +11,13 @@ namespace kvp {
 
 namespace {
 
+// Pool writes are streaming stores: left as ordinary dirty lines in the caches, the scattered page
+// blocks of a large append slow the next decode's streaming reads when they are evicted.
+__device__ __forceinline__ void store_stream(uint16_t* p, uint4 v) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4*>(p));
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
   __shared__ uint16_t vstage[4][16 * D];  // one page of V tokens per wave, [slot][dim]
@@ -35,7 +42,7 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
     const uint4 kk = *reinterpret_cast<const uint4*>(a.k + src);
     const uint4 vv = *reinterpret_cast<const uint4*>(a.v + src);
     const int s = r.s_lo + tt;
-    *reinterpret_cast<uint4*>(kblk + k_index<D>(s, c8 * 8)) = kk;
+    store_stream(kblk + k_index<D>(s, c8 * 8), kk);
     *reinterpret_cast<uint4*>(vs + s * D + c8 * 8) = vv;
   }
   __builtin_amdgcn_wave_barrier();
@@ -59,7 +66,7 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
       const int t = slot_token(8 * h + j);
       if (t >= r.s_lo && t < r.s_hi) val.s[j] = vs[t * D + dim];
     }
-    *reinterpret_cast<uint4*>(dst) = val.u;
+    store_stream(dst, val.u);
   }
 }
 
