@@ -107,7 +107,7 @@ def profiled_traffic(workload: str):
     return (int(float(dec)) if dec else None), (int(float(pf)) if pf else None)
 
 
-def library_gemm_tflops(dev, stream, n: int = 8192, reps: int = 10) -> float:
+def library_gemm_tflops(dev, stream, n: int = 16384, reps: int = 5) -> float:
     """bf16 dense GEMM rate of the vendor library (torch.matmul -> hipBLASLt) on N(0,1) operands.
 
     The chip's clock under dense bf16 matrix load depends on the operand data (random operands draw more
@@ -263,7 +263,7 @@ def main():
 
     traffic_dec, traffic_pf = profiled_traffic(args.workload)
     dec_bytes = decode_algorithmic_bytes(w)
-    dec_s = float(np.mean(t_dec)) / 1e3
+    dec_s = float(np.median(t_dec)) / 1e3
     dec_gbs = dec_bytes / dec_s / 1e9
     n_dec = int((w.decode_len > 0).sum())
     res = {
@@ -285,9 +285,10 @@ def main():
                    "logical_decode_tokens": w.logical_decode_tokens(), "seed": w.seed},
         "decode_hbm_peak_frac": round(dec_gbs / HBM_PEAK_GBS, 4),
         "decode_tokens_per_s": round(n_dec / dec_s, 1),
-        "decode_ms": {"mean": round(float(np.mean(t_dec)), 4), "p10": round(float(np.percentile(t_dec, 10)), 4),
+        "decode_ms": {"median": round(float(np.median(t_dec)), 4), "mean": round(float(np.mean(t_dec)), 4),
+                      "p10": round(float(np.percentile(t_dec, 10)), 4),
                       "p90": round(float(np.percentile(t_dec, 90)), 4)},
-        "append_ms": round(float(np.mean(t_app)), 4),
+        "append_ms": round(float(np.median(t_app)), 4),
         "hbm_copy_gbs": round(copy_gbs, 1),
         "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic_dec,
@@ -295,9 +296,10 @@ def main():
                      "algorithmic_bytes_per_launch": dec_bytes},
     }
     if has_prefill:
-        pf_s = float(np.mean(t_pf)) / 1e3
+        pf_s = float(np.median(t_pf)) / 1e3
         flops = w.prefill_flops()
-        res["prefill_ms"] = {"mean": round(float(np.mean(t_pf)), 4), "p10": round(float(np.percentile(t_pf, 10)), 4),
+        res["prefill_ms"] = {"median": round(float(np.median(t_pf)), 4), "mean": round(float(np.mean(t_pf)), 4),
+                             "p10": round(float(np.percentile(t_pf, 10)), 4),
                              "p90": round(float(np.percentile(t_pf, 90)), 4)}
         res["prefill_tflops"] = round(flops / pf_s / 1e12, 2)
         res["roofline_prefill"] = {"bound": "mfma", "achieved": round(flops / pf_s / 1e12, 2),

@@ -190,8 +190,7 @@ int upload_runs(const std::vector<kvp::PageRun>& runs, hipStream_t s, void** dev
 struct DecodeLayout {
   kvp::DecodePlan plan;
   Packer meta;
-  size_t off_wave = 0, off_seg = 0, off_group = 0, off_members = 0, off_part_base = 0, off_n_parts = 0,
-         off_merge = 0;
+  size_t off_wave = 0, off_seg = 0, off_group = 0, off_members = 0, off_part_base = 0, off_merge = 0;
   size_t off_acc = 0, off_ml = 0, total = 0;
 };
 
@@ -205,8 +204,16 @@ int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, con
   L->off_group = L->meta.add(P.group_items.data(), P.group_items.size() * sizeof(kvp::DecodeItem));
   L->off_members = L->meta.add(P.members.data(), P.members.size() * 4);
   L->off_part_base = L->meta.add(P.part_base.data(), P.part_base.size() * 4);
-  L->off_n_parts = L->meta.add(P.n_parts.data(), P.n_parts.size() * 4);
-  L->off_merge = L->meta.add(P.merge_seqs.data(), P.merge_seqs.size() * 4);
+  // One 16-byte record per merged sequence, so a merge workgroup starts from a single read.
+  std::vector<int32_t> info(4 * P.merge_seqs.size());
+  for (size_t k = 0; k < P.merge_seqs.size(); ++k) {
+    const int seq = P.merge_seqs[k];
+    info[4 * k] = seq;
+    info[4 * k + 1] = P.part_base[seq];
+    info[4 * k + 2] = P.n_parts[seq];
+    info[4 * k + 3] = 0;
+  }
+  L->off_merge = L->meta.add(info.data(), info.size() * 4);
   L->off_acc = 0;
   L->off_ml = L->off_acc + (((size_t)P.total_parts * Hq * pool->head_dim * 4 + 255) & ~size_t(255));
   L->total = L->off_ml + (((size_t)P.total_parts * Hq * 8 + 255) & ~size_t(255));
@@ -494,10 +501,8 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   hipError_t e = kvp::launch_decode(a, pool->head_dim, s);
   if (e == hipSuccess && !P.merge_seqs.empty()) {
     kvp::MergeArgs mg{};
-    mg.merge_seqs = reinterpret_cast<const int32_t*>(m + L.off_merge);
+    mg.merge_info = reinterpret_cast<const int32_t*>(m + L.off_merge);
     mg.n_merge = (int)P.merge_seqs.size();
-    mg.part_base = a.part_base;
-    mg.n_parts = reinterpret_cast<const int32_t*>(m + L.off_n_parts);
     mg.part_acc = a.part_acc;
     mg.part_ml = a.part_ml;
     mg.out = out;

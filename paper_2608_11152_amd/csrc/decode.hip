@@ -382,64 +382,88 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 // ---------------------------------------------------------------------------------------------------
 // Log-sum-exp merge: out = sum_j acc_j 2^(m_j - m) / sum_j l_j 2^(m_j - m), m = max_j m_j, in partial
 // order (fixed, so results are deterministic).  Empty partials (m = -inf, l = 0) carry zero weight; a
-// sequence with no partial gets a zero output.  One workgroup per (sequence, KV head): the G heads' max
-// and weight sum are reduced once into LDS (16 threads per head), then every thread accumulates four
-// consecutive output dims with 16-byte loads of the partial accumulators.
+// sequence with no partial gets a zero output.  One workgroup per (sequence, KV head), started from one
+// 16-byte record {seq, first partial, partial count}.  Phase 1: 16 threads per head hold up to four
+// partials' (m, l) each in registers, reduce the max and the weight sum, and leave each partial's weight
+// 2^(m_j - m) in LDS.  Phase 2: every thread accumulates four consecutive output dims over the partials
+// with up to 16 16-byte loads in flight.
 // ---------------------------------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
+  constexpr int MAXW = 64;  // partial weights per head kept in LDS; more partials recompute theirs
+  __shared__ float s_w[16][MAXW];
   __shared__ float s_m[16], s_inv[16];
-  const int seq = a.merge_seqs[blockIdx.x / a.Hkv];
-  const int kvh = blockIdx.x - (blockIdx.x / a.Hkv) * a.Hkv;
+  const int grp = blockIdx.x / a.Hkv;
+  const int kvh = blockIdx.x - grp * a.Hkv;
+  const int4 info = reinterpret_cast<const int4*>(a.merge_info)[grp];
+  const int seq = info.x, P = info.z;
+  const int64_t base = info.y;
   const int G = a.Hq / a.Hkv;
-  const int P = a.n_parts[seq];
-  const int64_t base = a.part_base[seq];
   const int tid = threadIdx.x;
   {
     const int hh = tid >> 4, r = tid & 15;
     const int h = kvh * G + hh;
+    const bool on = hh < G;
+    float2 ml[4];
     float m = -INFINITY;
-    if (hh < G)
-      for (int j = r; j < P; j += 16) m = fmaxf(m, a.part_ml[(base + j) * a.Hq + h].x);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int j = r + 16 * k;
+      ml[k] = (on && j < P) ? a.part_ml[(base + j) * a.Hq + h] : make_float2(-INFINITY, 0.0f);
+      m = fmaxf(m, ml[k].x);
+    }
+    if (on)
+      for (int j = r + 64; j < P; j += 16) m = fmaxf(m, a.part_ml[(base + j) * a.Hq + h].x);
 #pragma unroll
     for (int o = 8; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 16));
     float l = 0.0f;
-    if (hh < G && m != -INFINITY)
-      for (int j = r; j < P; j += 16) {
-        const float2 ml = a.part_ml[(base + j) * a.Hq + h];
-        l += fast_exp2(ml.x - m) * ml.y;
+    if (on && m != -INFINITY) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int j = r + 16 * k;
+        if (j < P) {
+          const float w = fast_exp2(ml[k].x - m);
+          l += w * ml[k].y;
+          s_w[hh][j] = w;
+        }
       }
+      for (int j = r + 64; j < P; j += 16) {
+        const float2 x = a.part_ml[(base + j) * a.Hq + h];
+        l += fast_exp2(x.x - m) * x.y;
+      }
+    }
 #pragma unroll
     for (int o = 8; o >= 1; o >>= 1) l += __shfl_xor(l, o, 16);
-    if (hh < G && r == 0) {
+    if (on && r == 0) {
       s_m[hh] = m;
       s_inv[hh] = (m != -INFINITY && l > 0.0f) ? 1.0f / l : 0.0f;
     }
   }
   __syncthreads();
   constexpr int V4 = D / 4;  // float4 per head row
+  constexpr int U = 16;      // partial loads in flight per thread
   for (int e = tid; e < G * V4; e += 256) {
     const int hh = e / V4, d4 = e - hh * V4;
     const int h = kvh * G + hh;
     const float m = s_m[hh], inv = s_inv[hh];
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     if (inv > 0.0f) {
-      const float2* ml = a.part_ml + base * a.Hq + h;
       const float* pa = a.part_acc + (base * a.Hq + h) * D + 4 * d4;
       const int64_t sa = (int64_t)a.Hq * D;
-      int j = 0;
-      for (; j + 4 <= P; j += 4) {  // four independent loads in flight, accumulated in partial order
-        f32x4 v[4];
-        float w[4];
+      for (int j0 = 0; j0 < P; j0 += U) {
+        f32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          v[u] = *reinterpret_cast<const f32x4*>(pa + (j + u) * sa);
-          w[u] = ml[(int64_t)(j + u) * a.Hq].x;
+        for (int u = 0; u < U; ++u)
+          if (j0 + u < P) v[u] = *reinterpret_cast<const f32x4*>(pa + (j0 + u) * sa);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int j = j0 + u;
+          if (j < P) {
+            const float w = j < MAXW ? s_w[hh][j] : fast_exp2(a.part_ml[(base + j) * a.Hq + h].x - m);
+            acc += w * v[u];
+          }
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) acc += fast_exp2(w[u] - m) * v[u];
       }
-      for (; j < P; ++j) acc += fast_exp2(ml[(int64_t)j * a.Hq].x - m) * *reinterpret_cast<const f32x4*>(pa + j * sa);
     }
     acc *= inv;
     const int64_t oi = ((int64_t)seq * a.Hq + h) * D + 4 * d4;

@@ -64,10 +64,8 @@ struct DecodeArgs {
 };
 
 struct MergeArgs {
-  const int32_t* merge_seqs;
+  const int32_t* merge_info;  // per merged sequence: {seq, first partial index, partial count, 0}
   int n_merge;
-  const int32_t* part_base;
-  const int32_t* n_parts;
   const float* part_acc;
   const float2* part_ml;
   void* out;
