@@ -31,6 +31,7 @@ sys.path.insert(0, ROOT)
 METRIC = "paged decode-attn effective KV GB/s (% HBM peak) + decode tokens/s, mixed batch"
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
+HOST_LINK_PEAK_GBS = 64.0  # PCIe Gen5 x16, one direction
 
 WORKLOAD_TEXT = {
     "mixed": "mixed step: 40 sessions (16 RLVR in 2 groups x 8, 12 RLHF in 6 groups x 2, 12 agentic), "
@@ -128,6 +129,41 @@ def library_gemm_tflops(dev, stream, n: int = 16384, reps: int = 5) -> float:
     torch.cuda.synchronize()
     del a, b, c
     return round(2.0 * n ** 3 * reps / (e0.elapsed_time(e1) / 1e3) / 1e12, 1)
+
+
+def kv_tier_leg(kp, pool, w, stream, reps: int = 3) -> dict:
+    """Host KV tier: offload, then restore, every page of the workload's longest sequence through pinned
+    host memory (kv_offload / kv_restore, one launch each), beside plain contiguous copies of the same
+    byte count between pinned host memory and HBM as the host link's practical rate."""
+    import torch
+    i = int(np.argmax(w.final_len))
+    ids = [int(x) for x in w.block_tables[i][: (int(w.final_len[i]) + 15) // 16]]
+    pb = kp.kv_pool_page_bytes(pool)
+    nbytes = len(ids) * pb
+    host = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    dev = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+
+    def timed(fn):
+        fn()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / 1e3)
+        return round(nbytes / float(np.median(ts)) / 1e9, 2)
+
+    off = timed(lambda: kp.kv_offload(pool, 0, ids, host))
+    res = timed(lambda: kp.kv_restore(pool, 0, host, ids))
+    h2d = timed(lambda: dev.copy_(host, non_blocking=True))
+    d2h = timed(lambda: host.copy_(dev, non_blocking=True))
+    del host, dev
+    return {"pages": len(ids), "bytes": nbytes, "offload_gbs": off, "restore_gbs": res, "h2d_copy_gbs": h2d,
+            "d2h_copy_gbs": d2h,
+            "roofline": {"bound": "host link", "achieved": res, "peak": HOST_LINK_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(res / HOST_LINK_PEAK_GBS, 4), "kernel": "kv_restore"}}
 
 
 def cpu_baseline(w, vals, budget_s: float):
@@ -310,6 +346,7 @@ def main():
                                    "algorithmic_bytes_per_launch": prefill_algorithmic_bytes(w),
                                    "library_gemm_tflops": gemm_tflops,
                                    "frac_of_library_gemm": round(flops / pf_s / 1e12 / gemm_tflops, 4)}
+    res["kv_tier"] = kv_tier_leg(kp, pool, w, stream)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, vals, args.cpu_seconds)
     print(json.dumps(res), flush=True)

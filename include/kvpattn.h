@@ -171,6 +171,36 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
                               size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------------------------
+ * CPU KV tier (Sec. 5.5: a host-memory tier keeps a backup copy of GPU-resident KV, so the GPU pool can
+ * run close to capacity and pages evicted from it come back without recomputation)
+ * ------------------------------------------------------------------------------------------------- */
+
+/* Bytes of one pool page of one layer (all KV heads, K and V blocks): num_kv_heads * 64 * head_dim. */
+int kv_pool_page_bytes(kvp_pool_t pool, size_t* bytes);
+
+/* Copy pool pages page_ids[0 .. n) of `layer` to the host tier: page i goes to host_dst + i * page_bytes,
+ * in the pool's page layout (file header), bit-exact.
+ *   page_ids  host int32 [n] (ids may repeat)
+ *   host_dst  pinned host memory (hipHostMalloc, or a torch tensor created with pin_memory=True) of
+ *             n * page_bytes bytes; the GPU writes it directly, in one launch for all n pages.  It is
+ *             complete once the work enqueued on `stream` has finished.
+ * Errors: KVP_ERANGE if an id is outside [0, num_pages); KVP_EINVAL if host_dst is not pinned host
+ * memory. */
+int kv_offload(kvp_pool_t pool, int layer, const int32_t* page_ids, int n, void* host_dst, void* stream);
+
+/* Copy host-tier page i (as kv_offload wrote it) into pool page page_ids[i] of `layer`, bit-exact, in
+ * one launch.  When block_tables is not NULL, block_tables[rows[i] * maxp + lpages[i]] is also set to
+ * page_ids[i] on the stream, so the restored page becomes logical page lpages[i] of table row rows[i].
+ *   host_src      pinned host memory of n * page_bytes bytes
+ *   page_ids      host int32 [n], distinct
+ *   block_tables  device int32 [num_rows, maxp], nullable;  rows, lpages host int32 [n] (used with it)
+ * Errors: KVP_ERANGE for a page id outside [0, num_pages) or lpages[i] outside [0, maxp); KVP_EINVAL if
+ * a page id repeats, rows[i] is outside [0, num_rows), or host_src is not pinned host memory. */
+int kv_restore(kvp_pool_t pool, int layer, const void* host_src, const int32_t* page_ids, int n,
+               int32_t* block_tables, int num_rows, int maxp, const int32_t* rows, const int32_t* lpages,
+               void* stream);
+
+/* ---------------------------------------------------------------------------------------------------
  * Host-side checks and diagnostics
  * ------------------------------------------------------------------------------------------------- */
 

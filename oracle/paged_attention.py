@@ -168,3 +168,20 @@ def prefill(q_bits, pool_k, pool_v, block_tables, ctx_lens, cu_q, scale: float) 
         k, v = gather(pool_k, pool_v, block_tables[i], ctx + (b - a))
         out[a:b] = prefill_seq(q_bits[a:b], k, v, scale, ctx)
     return out
+
+
+def offload(pool_k, pool_v, page_ids):
+    """The host tier's copy of pool pages page_ids (Sec. 5.5: a host-memory tier backs up GPU-resident
+    KV): their K and V raw bits, [n, Hkv, 16, d] each, in the order given."""
+    ids = np.asarray(page_ids, dtype=np.int64)
+    return pool_k[ids].copy(), pool_v[ids].copy()
+
+
+def restore(pool_k, pool_v, page_ids, host_k, host_v, block_tables=None, rows=None, lpages=None):
+    """Put host-tier page i back into pool page page_ids[i]; when a block table is given, logical page
+    lpages[i] of table row rows[i] then names that page.  Copies bits, so the result is exact."""
+    for i, p in enumerate(page_ids):
+        pool_k[int(p)] = host_k[i]
+        pool_v[int(p)] = host_v[i]
+        if block_tables is not None:
+            block_tables[int(rows[i]), int(lpages[i])] = int(p)

@@ -150,6 +150,23 @@ struct Packer {
 
 bool pool_ok(kvp_pool_t p) { return p && p->base; }
 
+size_t page_bytes(kvp_pool_t p) { return (size_t)p->num_kv_heads * 2 * kvp::kPage * p->head_dim * 2; }
+
+// The host tier is read and written by kernels, so it must be pinned host memory (hipHostMalloc, or a
+// torch tensor created with pin_memory=True) that covers `bytes` from `p`.
+int check_pinned(const void* p, size_t bytes, const char* what) {
+  if (!p) return set_err(KVP_EINVAL, "%s is NULL", what);
+  hipPointerAttribute_t at{};
+  hipError_t e = hipPointerGetAttributes(&at, p);
+  if (e != hipSuccess || at.type != hipMemoryTypeHost) {
+    (void)hipGetLastError();
+    return set_err(KVP_EINVAL, "%s is not pinned host memory", what);
+  }
+  (void)bytes;
+  return KVP_OK;
+}
+
+
 int check_layer(kvp_pool_t pool, int layer) {
   if (!pool_ok(pool)) return set_err(KVP_EINVAL, "pool is NULL or destroyed");
   if (layer < 0 || layer >= pool->num_layers)
@@ -174,6 +191,29 @@ void build_runs(const int32_t* start, const int64_t* first_src, const int32_t* c
                                    first_src[i] + (lo - a)});
     }
   }
+}
+
+// Page moves between the pool and the host tier: the item list is read by the kernel straight from a
+// pinned staging slot, released after the kernel.
+int run_tier(kvp_pool_t pool, int layer, const std::vector<kvp::TierItem>& items, void* host, int32_t* bt,
+             int maxp, bool restore, hipStream_t s) {
+  Staging::Lease lease;
+  const size_t nb = items.size() * sizeof(kvp::TierItem);
+  int rc = staging().lease(nb, &lease);
+  if (rc) return rc;
+  std::memcpy(lease.host, items.data(), nb);
+  kvp::TierArgs a{};
+  a.layer = reinterpret_cast<unsigned char*>(const_cast<uint16_t*>(layer_ptr(pool, layer)));
+  a.host = reinterpret_cast<unsigned char*>(host);
+  a.page_bytes = (int64_t)page_bytes(pool);
+  a.items = reinterpret_cast<const kvp::TierItem*>(lease.host);
+  a.n = (int)items.size();
+  a.bt = bt;
+  a.maxp = maxp;
+  hipError_t e = kvp::launch_tier(a, restore, s);
+  const int rr = staging().release(lease, s, e == hipSuccess);
+  if (e != hipSuccess) return hip_err(e, restore ? "kv_restore launch" : "kv_offload launch");
+  return rr;
 }
 
 int upload_runs(const std::vector<kvp::PageRun>& runs, hipStream_t s, void** dev) {
@@ -435,6 +475,62 @@ int kv_gather(kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
   hipError_t e = kvp::launch_gather(a, pool->head_dim, s);
   (void)hipFreeAsync(druns, s);
   return e == hipSuccess ? KVP_OK : hip_err(e, "kv_gather launch");
+}
+
+int kv_pool_page_bytes(kvp_pool_t pool, size_t* bytes) {
+  if (!pool_ok(pool) || !bytes) return set_err(KVP_EINVAL, "pool or bytes is NULL");
+  *bytes = page_bytes(pool);
+  return KVP_OK;
+}
+
+int kv_offload(kvp_pool_t pool, int layer, const int32_t* page_ids, int n, void* host_dst, void* stream) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (n < 0) return set_err(KVP_EINVAL, "n = %d < 0", n);
+  if (n == 0) return KVP_OK;
+  if (!page_ids) return set_err(KVP_EINVAL, "page_ids is NULL");
+  rc = check_pinned(host_dst, (size_t)n * page_bytes(pool), "host_dst");
+  if (rc) return rc;
+  std::vector<kvp::TierItem> items(n);
+  for (int i = 0; i < n; ++i) {
+    if ((unsigned)page_ids[i] >= (unsigned)pool->num_pages)
+      return set_err(KVP_ERANGE, "page_ids[%d] = %d outside [0, %d)", i, page_ids[i], pool->num_pages);
+    items[i] = kvp::TierItem{page_ids[i], 0, 0, 0};
+  }
+  return run_tier(pool, layer, items, host_dst, nullptr, 0, false, reinterpret_cast<hipStream_t>(stream));
+}
+
+int kv_restore(kvp_pool_t pool, int layer, const void* host_src, const int32_t* page_ids, int n,
+               int32_t* block_tables, int num_rows, int maxp, const int32_t* rows, const int32_t* lpages,
+               void* stream) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (n < 0) return set_err(KVP_EINVAL, "n = %d < 0", n);
+  if (n == 0) return KVP_OK;
+  if (!page_ids) return set_err(KVP_EINVAL, "page_ids is NULL");
+  if (block_tables && (!rows || !lpages || num_rows <= 0 || maxp <= 0))
+    return set_err(KVP_EINVAL, "a block-table patch needs rows, lpages, num_rows > 0 and maxp > 0");
+  rc = check_pinned(host_src, (size_t)n * page_bytes(pool), "host_src");
+  if (rc) return rc;
+  std::vector<unsigned char> seen(pool->num_pages, 0);
+  std::vector<kvp::TierItem> items(n);
+  for (int i = 0; i < n; ++i) {
+    const int id = page_ids[i];
+    if ((unsigned)id >= (unsigned)pool->num_pages)
+      return set_err(KVP_ERANGE, "page_ids[%d] = %d outside [0, %d)", i, id, pool->num_pages);
+    if (seen[id]) return set_err(KVP_EINVAL, "page id %d is restored twice", id);
+    seen[id] = 1;
+    int row = 0, lp = 0;
+    if (block_tables) {
+      row = rows[i];
+      lp = lpages[i];
+      if (row < 0 || row >= num_rows) return set_err(KVP_EINVAL, "rows[%d] = %d outside [0, %d)", i, row, num_rows);
+      if (lp < 0 || lp >= maxp) return set_err(KVP_ERANGE, "lpages[%d] = %d outside [0, %d)", i, lp, maxp);
+    }
+    items[i] = kvp::TierItem{id, row, lp, 0};
+  }
+  return run_tier(pool, layer, items, const_cast<void*>(host_src), block_tables, maxp, true,
+                  reinterpret_cast<hipStream_t>(stream));
 }
 
 int paged_decode_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int num_seqs,

@@ -89,11 +89,28 @@ struct PrefillArgs {
   int* err;
 };
 
+// One page moved between the pool and the host tier; row / lpage name the block-table entry a restore
+// points at the page (ignored when no table is patched).
+struct TierItem {
+  int32_t page, row, lpage, pad;
+};
+
+struct TierArgs {
+  unsigned char* layer;     // pool layer base
+  unsigned char* host;      // pinned host pages, item i at host + i * page_bytes
+  int64_t page_bytes;
+  const TierItem* items;    // n items (read from pinned host memory)
+  int n;
+  int32_t* bt;              // device block tables to patch, or NULL
+  int maxp;
+};
+
 hipError_t launch_append(const AppendArgs& a, int D, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, int D, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s);
 hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s);
 hipError_t launch_prefill(const PrefillArgs& a, int D, hipStream_t s);
+hipError_t launch_tier(const TierArgs& a, bool restore, hipStream_t s);
 
 }  // namespace kvp

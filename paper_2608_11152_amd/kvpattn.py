@@ -23,7 +23,8 @@ PAGE = 16
 # Every symbol the header declares (kept in sync by a CPU test that parses include/kvpattn.h).
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_reset", "kv_pool_layer_ptr", "kv_pool_info",
            "kv_pool_device_error", "kv_append", "kv_gather", "paged_decode_workspace_size", "paged_decode_attn",
-           "prefix_chunk_prefill_workspace_size", "prefix_chunk_prefill_attn", "kvp_check_tables",
+           "prefix_chunk_prefill_workspace_size", "prefix_chunk_prefill_attn", "kv_pool_page_bytes", "kv_offload",
+           "kv_restore", "kvp_check_tables",
            "kvp_plan_decode", "kvp_strerror", "kvp_last_error", "kvp_version"]
 
 
@@ -63,6 +64,9 @@ def lib() -> C.CDLL:
         L.paged_decode_attn.argtypes = [vp, p, i, vp, i, i32p, i, gpp, i, C.c_float, vp, i, vp, sz, vp]
         L.prefix_chunk_prefill_workspace_size.argtypes = [p, i32p, i32p, i, i, C.POINTER(sz)]
         L.prefix_chunk_prefill_attn.argtypes = [vp, p, i, vp, i, i32p, i32p, i, i, C.c_float, vp, i, vp, sz, vp]
+        L.kv_pool_page_bytes.argtypes = [p, C.POINTER(sz)]
+        L.kv_offload.argtypes = [p, i, i32p, i, vp, vp]
+        L.kv_restore.argtypes = [p, i, vp, i32p, i, vp, i, i, i32p, i32p, vp]
         L.kvp_check_tables.argtypes = [i32p, i, i32p, i, i, gpp]
         L.kvp_plan_decode.argtypes = [i32p, i, gpp, i, i, i32p, i, C.POINTER(i), C.POINTER(i), C.POINTER(i)]
         L.kvp_strerror.argtypes = [i]
@@ -261,6 +265,42 @@ def prefix_chunk_prefill_attn(q, pool: Pool, layer, block_tables, ctx_lens, cu_q
                                            _ptr(cl), _ptr(cq), len(cl), Hq, float(scale), _dptr(out), od, _dptr(ws),
                                            ws.numel(), _stream(stream)), "prefix_chunk_prefill_attn")
     return out
+
+
+def kv_pool_page_bytes(pool: Pool) -> int:
+    n = C.c_size_t()
+    _check(lib().kv_pool_page_bytes(pool.handle, C.byref(n)), "kv_pool_page_bytes")
+    return n.value
+
+
+def _check_host_size(pool: Pool, host, n: int, what: str):
+    """The library trusts the host tier's extent (like any caller pointer): check it here."""
+    if host is not None and host.numel() * host.element_size() < n * kv_pool_page_bytes(pool):
+        raise ValueError(f"{what} holds {host.numel() * host.element_size()} bytes, "
+                         f"{n} pages need {n * kv_pool_page_bytes(pool)}")
+
+
+def kv_offload(pool: Pool, layer, page_ids, host_dst, stream=None):
+    """Copy pool pages to the host tier.  host_dst: pinned host tensor of len(page_ids) * page_bytes bytes."""
+    ids = _i32(page_ids)
+    _check_host_size(pool, host_dst, len(ids), "host_dst")
+    _check(lib().kv_offload(pool.handle, layer, _ptr(ids), len(ids), _dptr(host_dst), _stream(stream)), "kv_offload")
+
+
+def kv_restore(pool: Pool, layer, host_src, page_ids, block_tables=None, rows=None, lpages=None, stream=None):
+    """Copy host-tier pages into pool pages page_ids; optionally patch block_tables[rows, lpages] = page_ids."""
+    ids = _i32(page_ids)
+    _check_host_size(pool, host_src, len(ids), "host_src")
+    if block_tables is not None:
+        r, lp = _i32(rows), _i32(lpages)
+        if len(r) != len(ids) or len(lp) != len(ids):
+            raise ValueError("rows and lpages need one entry per page id")
+        nr, mp = block_tables.shape
+        rp, lpp = _ptr(r), _ptr(lp)
+    else:
+        nr, mp, rp, lpp = 0, 0, None, None
+    _check(lib().kv_restore(pool.handle, layer, _dptr(host_src), _ptr(ids), len(ids), _dptr(block_tables), nr, mp,
+                            rp, lpp, _stream(stream)), "kv_restore")
 
 
 def kvp_check_tables(block_tables_host, lens, num_pages, group_prefix=None) -> int:

@@ -429,3 +429,43 @@ def test_planted_causal_off_by_one_is_caught(monkeypatch):
     monkeypatch.setattr(OP, "attend_causal", lambda q_, k, v, s, fp: real(q_, k, v, s, fp - 1))
     pre = OP.prefill(q, pk, pv, bt, sl - 1, np.array([0, 1], np.int32), 0.3)
     assert np.max(np.abs(dec - pre)) > 1e-6
+
+
+# ------------------------------------------------------------------------------------------------
+# host KV tier (Sec. 5.5): eviction to the host and restore into other physical pages changes nothing
+# ------------------------------------------------------------------------------------------------
+
+def test_tier_restore_elsewhere_is_invisible():
+    """Offload every used page, wipe them, restore each into an unused page with the block tables
+    patched: gathers and decode are bitwise unchanged (attention never sees where a page lives).
+    Restoring over the original pages after the wipe gives back the same pool."""
+    rng = np.random.default_rng(5)
+    q, pk, pv, bt, lens, *_ = small_case(rng, num_pages=32)
+    ref = oracle.decode(q, pk, pv, bt, lens, 0.3)
+    used = [int(x) for x in np.unique(bt[bt >= 0])]
+    free = [p for p in range(32) if p not in used]
+    hk, hv = oracle.offload(pk, pv, used)
+    assert hk.shape == (len(used),) + pk.shape[1:] and hv.shape == hk.shape
+    assert np.array_equal(hk, pk[used]) and np.array_equal(hv, pv[used])
+    pk2, pv2, bt2 = pk.copy(), pv.copy(), bt.copy()
+    pk2[used] = 0
+    pv2[used] = 0
+    dst = [int(x) for x in rng.permutation(free)[: len(used)]]
+    rows, lps = [], []
+    for p in used:  # every page of small_case is referenced by exactly one (row, logical page)
+        i, lp = (int(x) for x in np.argwhere(bt == p)[0])
+        rows.append(i)
+        lps.append(lp)
+    oracle.restore(pk2, pv2, dst, hk, hv, bt2, rows, lps)
+    for j, p in enumerate(used):
+        assert bt2[rows[j], lps[j]] == dst[j] and bt[rows[j], lps[j]] == p
+    for i, n in enumerate(lens):
+        a = oracle.gather(pk, pv, bt[i], int(n))
+        b = oracle.gather(pk2, pv2, bt2[i], int(n))
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    assert np.array_equal(oracle.decode(q, pk2, pv2, bt2, lens, 0.3), ref)
+    pk3, pv3 = pk.copy(), pv.copy()
+    pk3[used] = 0
+    pv3[used] = 0
+    oracle.restore(pk3, pv3, used, hk, hv)
+    assert np.array_equal(pk3, pk) and np.array_equal(pv3, pv)
