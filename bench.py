@@ -166,6 +166,48 @@ def kv_tier_leg(kp, pool, w, stream, reps: int = 3) -> dict:
                          "frac": round(res / HOST_LINK_PEAK_GBS, 4), "kernel": "kv_restore"}}
 
 
+def prefix_hash_leg(kp, W, w, stream, reps: int = 5) -> dict:
+    """Prompt-block hashing and prefix lookup over the workload's synthetic token ids: hash every full
+    page of every sequence, derive the groups' shared pages, register each sequence's cached history in
+    a device prefix table, and look up the full sequences (their reusable prefix H)."""
+    import torch
+    tokens, cu = W.make_tokens(w)
+    th, cuh = W.make_tokens(w, lens=W.step_start(w))
+    t_dev, th_dev = torch.from_numpy(tokens).cuda(), torch.from_numpy(th).cuda()
+    off_h = kp.block_hash_offsets(cuh)
+    ids = np.concatenate([w.block_tables[i][: int(off_h[i + 1] - off_h[i])] for i in range(w.B)]).astype(np.int32)
+    ids_dev = torch.from_numpy(ids).cuda()
+    pages = int(kp.block_hash_offsets(cu)[-1])
+    h_all = torch.empty(max(1, pages), dtype=torch.int64, device="cuda")
+    table = kp.PrefixTable(max(10, int(np.ceil(np.log2(max(2, 2 * len(ids)))))))
+    h_hist = kp.kvp_block_hashes(th_dev, cuh)
+    table.insert(h_hist, ids_dev)
+
+    def timed(fn):
+        fn()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    t_hash = timed(lambda: kp.kvp_block_hashes(t_dev, cu, out=h_all))
+    t_look = timed(lambda: table.lookup(h_all, cu))
+    matched, _ = table.lookup(h_all, cu)
+    shared = kp.kvp_group_shared_pages(h_all, cu, w.group_id, w.num_groups) if w.num_groups else np.zeros(0)
+    ok = bool(np.array_equal(shared, w.shared_pages)) and bool(
+        np.array_equal(matched.cpu().numpy(), W.step_start(w) // 16))
+    table.close()
+    return {"tokens": int(cu[-1]), "pages": pages, "hash_ms": round(t_hash, 4),
+            "hash_tokens_per_s": round(int(cu[-1]) / (t_hash / 1e3), 1), "lookup_ms": round(t_look, 4),
+            "lookup_pages_per_s": round(pages / (t_look / 1e3), 1), "reused_tokens": int(matched.sum().item()) * 16,
+            "derived_prefixes_match": ok}
+
+
 def cpu_baseline(w, vals, budget_s: float):
     """Time the CPU fp64 oracle (as it stands) on a bounded sample of the same decode workload."""
     import oracle
@@ -347,6 +389,7 @@ def main():
                                    "library_gemm_tflops": gemm_tflops,
                                    "frac_of_library_gemm": round(flops / pf_s / 1e12 / gemm_tflops, 4)}
     res["kv_tier"] = kv_tier_leg(kp, pool, w, stream)
+    res["prefix_hash"] = prefix_hash_leg(kp, W, w, stream)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, vals, args.cpu_seconds)
     print(json.dumps(res), flush=True)

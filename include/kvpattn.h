@@ -201,6 +201,67 @@ int kv_restore(kvp_pool_t pool, int layer, const void* host_src, const int32_t* 
                void* stream);
 
 /* ---------------------------------------------------------------------------------------------------
+ * Prompt-block hashing and prefix lookup (Sec. 4.4: the engine names every full prompt block by a hash,
+ * and the longest matching prompt-block hash is a request's reusable prefix H of Eq. 1)
+ *
+ * Block hash (the paper does not specify one; this is the library's definition, all arithmetic mod 2^64):
+ *   mix(z)   = SplitMix64 output function: z += 0x9E3779B97F4A7C15; z = (z ^ z>>30) * 0xBF58476D1CE4E5B9;
+ *              z = (z ^ z>>27) * 0x94D049BB133111EB; z ^= z>>31
+ *   local(k) = x after x = mix(x ^ (t[16k+2j] | t[16k+2j+1] << 32)) for j = 0..7, from x = 0
+ *              (token ids as uint32)
+ *   h(-1) = seed;  h(k) = h(k-1) * 0x9E3779B97F4A7C15 + local(k);  hash(k) = mix(h(k))
+ * so hash(k) names the tokens [0, 16(k+1)) of a sequence: equal prefixes give equal hashes.  Only full
+ * pages are hashed.  Hash slots are laid out per sequence: sequence i's floor(len_i / 16) hashes start
+ * at sum_{j<i} floor(len_j / 16), with len_i = cu_tokens[i+1] - cu_tokens[i].
+ * ------------------------------------------------------------------------------------------------- */
+
+/* Block hashes of every full page of every sequence.
+ *   tokens     device int32 [cu_tokens[num_seqs]] (token ids, sequences concatenated)
+ *   cu_tokens  host int32 [num_seqs + 1], non-decreasing, cu_tokens[0] = 0
+ *   hashes     device uint64 [total full pages] (layout above) */
+int kvp_block_hashes(const int32_t* tokens, const int32_t* cu_tokens, int num_seqs, uint64_t seed,
+                     uint64_t* hashes, void* stream);
+
+/* Rollout-group shared prefix from block hashes: shared_pages[g] (device int32 [num_groups]) = the
+ * number of leading full pages on which every member of group g has the same hash as its first member,
+ * capped by the shortest member (0 for a group without members).  With the groups' prompt tokens this is
+ * the kvp_group_prefix.shared_pages of decode (whole pages only).
+ *   hashes, cu_tokens  as written by kvp_block_hashes;  group_id host int32 [num_seqs], -1 = ungrouped.
+ * Errors: KVP_EGROUP for a group id outside [-1, num_groups). */
+int kvp_group_shared_pages(const uint64_t* hashes, const int32_t* cu_tokens, int num_seqs,
+                           const int32_t* group_id, int num_groups, int32_t* shared_pages, void* stream);
+
+typedef struct kvp_prefix_table* kvp_prefix_table_t; /* device hash table: block hash -> pool page */
+
+/* An empty table of 2^capacity_log2 slots (4..30) in device memory, 12 bytes per slot.
+ * Open addressing with linear probing; a slot's page is the largest page id inserted for its hash, or
+ * -1 after that page was erased.  A block hash of 0 is stored as 1. */
+int kvp_prefix_table_create(kvp_prefix_table_t* out, int capacity_log2);
+int kvp_prefix_table_destroy(kvp_prefix_table_t table);
+
+/* Empty the table on `stream` (the cache reset after a weight sync, Sec. 5.2). */
+int kvp_prefix_table_clear(kvp_prefix_table_t table, void* stream);
+
+/* Record that pool page page_ids[i] holds the block named hashes[i] (device arrays of n entries).  When
+ * the table is full an entry is dropped and kvp_prefix_table_error reports KVP_ENOMEM. */
+int kvp_prefix_table_insert(kvp_prefix_table_t table, const uint64_t* hashes, const int32_t* page_ids,
+                            int64_t n, void* stream);
+
+/* Forget that page page_ids[i] holds block hashes[i] (a page evicted from the pool); entries that map
+ * the hash to another page are left alone. */
+int kvp_prefix_table_erase(kvp_prefix_table_t table, const uint64_t* hashes, const int32_t* page_ids,
+                           int64_t n, void* stream);
+
+/* Reusable prefix of each sequence: matched_pages[i] (device int32 [num_seqs]) = the number of leading
+ * full pages whose hash the table maps to a page; page_ids (device int32 [total full pages], layout above)
+ * receives those pages and -1 after the first miss.  H = 16 * matched_pages[i] tokens need no prefill. */
+int kvp_prefix_lookup(kvp_prefix_table_t table, const uint64_t* hashes, const int32_t* cu_tokens,
+                      int num_seqs, int32_t* matched_pages, int32_t* page_ids, void* stream);
+
+/* Synchronise the device, then return (in *code) and clear the table's device error word. */
+int kvp_prefix_table_error(kvp_prefix_table_t table, int* code);
+
+/* ---------------------------------------------------------------------------------------------------
  * Host-side checks and diagnostics
  * ------------------------------------------------------------------------------------------------- */
 

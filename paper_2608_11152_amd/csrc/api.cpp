@@ -15,6 +15,14 @@
 
 #include "kvp_kernels.h"
 
+struct kvp_prefix_table {
+  uint64_t* keys = nullptr;
+  int32_t* vals = nullptr;
+  uint64_t mask = 0;
+  int* err = nullptr;
+  int device = 0;
+};
+
 struct kvp_pool {
   int num_layers = 0, num_pages = 0, num_kv_heads = 0, head_dim = 0, device = 0;
   size_t layer_bytes = 0;
@@ -191,6 +199,34 @@ void build_runs(const int32_t* start, const int64_t* first_src, const int32_t* c
                                    first_src[i] + (lo - a)});
     }
   }
+}
+
+// Per-sequence {first token, full pages, first hash slot, 0} from host cu_tokens, in a leased pinned slot
+// (appended after `extra` bytes the caller packs first).  Returns the total full-page count in *pages.
+int lease_seq_info(const int32_t* cu_tokens, int num_seqs, Staging::Lease* lease, int64_t* pages,
+                   const std::vector<unsigned char>& extra, size_t* info_off) {
+  if (num_seqs > 0 && !cu_tokens) return set_err(KVP_EINVAL, "cu_tokens is NULL");
+  if (num_seqs > 0 && cu_tokens[0] != 0) return set_err(KVP_EINVAL, "cu_tokens[0] = %d, must be 0", cu_tokens[0]);
+  std::vector<int32_t> info(4 * (size_t)num_seqs);
+  int64_t tot = 0;
+  for (int i = 0; i < num_seqs; ++i) {
+    const int32_t n = cu_tokens[i + 1] - cu_tokens[i];
+    if (n < 0) return set_err(KVP_EINVAL, "cu_tokens decreases at %d", i);
+    info[4 * i] = cu_tokens[i];
+    info[4 * i + 1] = n / kvp::kPage;
+    info[4 * i + 2] = (int32_t)tot;
+    info[4 * i + 3] = 0;
+    tot += n / kvp::kPage;
+    if (tot > INT32_MAX) return set_err(KVP_EINVAL, "more than 2^31 pages");
+  }
+  *pages = tot;
+  const size_t off = (extra.size() + 255) & ~size_t(255);
+  int rc = staging().lease(std::max<size_t>(1, off + info.size() * 4), lease);
+  if (rc) return rc;
+  if (!extra.empty()) std::memcpy(lease->host, extra.data(), extra.size());
+  if (!info.empty()) std::memcpy(reinterpret_cast<unsigned char*>(lease->host) + off, info.data(), info.size() * 4);
+  *info_off = off;
+  return KVP_OK;
 }
 
 // Page moves between the pool and the host tier: the item list is read by the kernel straight from a
@@ -531,6 +567,200 @@ int kv_restore(kvp_pool_t pool, int layer, const void* host_src, const int32_t* 
   }
   return run_tier(pool, layer, items, const_cast<void*>(host_src), block_tables, maxp, true,
                   reinterpret_cast<hipStream_t>(stream));
+}
+
+int kvp_block_hashes(const int32_t* tokens, const int32_t* cu_tokens, int num_seqs, uint64_t seed,
+                     uint64_t* hashes, void* stream) {
+  if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
+  if (num_seqs == 0) return KVP_OK;
+  Staging::Lease lease;
+  int64_t pages = 0;
+  size_t off = 0;
+  int rc = lease_seq_info(cu_tokens, num_seqs, &lease, &pages, {}, &off);
+  if (rc) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (pages == 0) return staging().release(lease, s, false);
+  if (!tokens || !hashes) {
+    (void)staging().release(lease, s, false);
+    return set_err(KVP_EINVAL, "tokens or hashes is NULL");
+  }
+  kvp::HashArgs a{};
+  a.tokens = tokens;
+  a.seq_info = reinterpret_cast<const int4*>(reinterpret_cast<unsigned char*>(lease.host) + off);
+  a.seed = seed;
+  a.out = hashes;
+  hipError_t e = kvp::launch_block_hash(a, num_seqs, s);
+  const int rr = staging().release(lease, s, e == hipSuccess);
+  if (e != hipSuccess) return hip_err(e, "kvp_block_hashes launch");
+  return rr;
+}
+
+int kvp_group_shared_pages(const uint64_t* hashes, const int32_t* cu_tokens, int num_seqs, const int32_t* group_id,
+                           int num_groups, int32_t* shared_pages, void* stream) {
+  if (num_seqs < 0 || num_groups < 0) return set_err(KVP_EINVAL, "negative count");
+  if (num_groups == 0) return KVP_OK;
+  if (!group_id || !shared_pages) return set_err(KVP_EINVAL, "group_id or shared_pages is NULL");
+  std::vector<int32_t> cnt(num_groups + 1, 0);
+  for (int i = 0; i < num_seqs; ++i) {
+    const int g = group_id[i];
+    if (g < -1 || g >= num_groups) return set_err(KVP_EGROUP, "group_id[%d] = %d outside [-1, %d)", i, g, num_groups);
+    if (g >= 0) ++cnt[g + 1];
+  }
+  for (int g = 0; g < num_groups; ++g) cnt[g + 1] += cnt[g];
+  std::vector<int32_t> members(std::max(1, cnt[num_groups])), fill(cnt.begin(), cnt.end() - 1);
+  for (int i = 0; i < num_seqs; ++i)
+    if (group_id[i] >= 0) members[fill[group_id[i]]++] = i;
+  // pinned slot: [grp_off | members | seq_info]
+  std::vector<unsigned char> extra;
+  const size_t moff = ((cnt.size() * 4) + 255) & ~size_t(255);
+  extra.resize(moff + members.size() * 4);
+  std::memcpy(extra.data(), cnt.data(), cnt.size() * 4);
+  std::memcpy(extra.data() + moff, members.data(), members.size() * 4);
+  Staging::Lease lease;
+  int64_t pages = 0;
+  size_t off = 0;
+  int rc = lease_seq_info(cu_tokens, num_seqs, &lease, &pages, extra, &off);
+  if (rc) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (pages > 0 && !hashes) {
+    (void)staging().release(lease, s, false);
+    return set_err(KVP_EINVAL, "hashes is NULL");
+  }
+  const unsigned char* h = reinterpret_cast<const unsigned char*>(lease.host);
+  kvp::GroupLcpArgs a{};
+  a.hashes = hashes;
+  a.seq_info = reinterpret_cast<const int4*>(h + off);
+  a.grp_off = reinterpret_cast<const int32_t*>(h);
+  a.members = reinterpret_cast<const int32_t*>(h + moff);
+  a.shared_pages = shared_pages;
+  hipError_t e = kvp::launch_group_lcp(a, num_groups, s);
+  const int rr = staging().release(lease, s, e == hipSuccess);
+  if (e != hipSuccess) return hip_err(e, "kvp_group_shared_pages launch");
+  return rr;
+}
+
+int kvp_prefix_table_create(kvp_prefix_table_t* out, int capacity_log2) {
+  if (!out) return set_err(KVP_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (capacity_log2 < 4 || capacity_log2 > 30) return set_err(KVP_EINVAL, "capacity_log2 %d outside [4, 30]", capacity_log2);
+  auto* t = new kvp_prefix_table();
+  const size_t cap = size_t(1) << capacity_log2;
+  t->mask = cap - 1;
+  hipError_t e = hipGetDevice(&t->device);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&t->keys), cap * 8);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&t->vals), cap * 4);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&t->err), 256);
+  if (e == hipSuccess) {
+    kvp::TableArgs a{};
+    a.keys = t->keys;
+    a.vals = t->vals;
+    a.mask = t->mask;
+    e = kvp::launch_table(a, 3, 0, nullptr);
+  }
+  if (e == hipSuccess) e = kvp::launch_fill_zero(t->err, 256, nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    (void)hipFree(t->keys);
+    (void)hipFree(t->vals);
+    (void)hipFree(t->err);
+    delete t;
+    return set_err(KVP_ENOMEM, "prefix table of 2^%d slots: %s", capacity_log2, hipGetErrorString(e));
+  }
+  *out = t;
+  return KVP_OK;
+}
+
+int kvp_prefix_table_destroy(kvp_prefix_table_t t) {
+  if (!t) return KVP_OK;
+  (void)hipDeviceSynchronize();
+  (void)hipFree(t->keys);
+  (void)hipFree(t->vals);
+  (void)hipFree(t->err);
+  delete t;
+  return KVP_OK;
+}
+
+int kvp_prefix_table_clear(kvp_prefix_table_t t, void* stream) {
+  if (!t) return set_err(KVP_EINVAL, "table is NULL");
+  kvp::TableArgs a{};
+  a.keys = t->keys;
+  a.vals = t->vals;
+  a.mask = t->mask;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = kvp::launch_table(a, 3, 0, s);
+  if (e == hipSuccess) e = kvp::launch_fill_zero(t->err, 256, s);
+  return e == hipSuccess ? KVP_OK : hip_err(e, "kvp_prefix_table_clear launch");
+}
+
+static int table_update(kvp_prefix_table_t t, const uint64_t* hashes, const int32_t* page_ids, int64_t n, int op,
+                        void* stream) {
+  if (!t) return set_err(KVP_EINVAL, "table is NULL");
+  if (n < 0) return set_err(KVP_EINVAL, "n < 0");
+  if (n == 0) return KVP_OK;
+  if (!hashes || !page_ids) return set_err(KVP_EINVAL, "hashes or page_ids is NULL");
+  kvp::TableArgs a{};
+  a.keys = t->keys;
+  a.vals = t->vals;
+  a.mask = t->mask;
+  a.hashes = hashes;
+  a.pages = page_ids;
+  a.n = n;
+  a.err = t->err;
+  hipError_t e = kvp::launch_table(a, op, 0, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? KVP_OK : hip_err(e, "prefix table launch");
+}
+
+int kvp_prefix_table_insert(kvp_prefix_table_t t, const uint64_t* hashes, const int32_t* page_ids, int64_t n,
+                            void* stream) {
+  return table_update(t, hashes, page_ids, n, 0, stream);
+}
+
+int kvp_prefix_table_erase(kvp_prefix_table_t t, const uint64_t* hashes, const int32_t* page_ids, int64_t n,
+                           void* stream) {
+  return table_update(t, hashes, page_ids, n, 1, stream);
+}
+
+int kvp_prefix_lookup(kvp_prefix_table_t t, const uint64_t* hashes, const int32_t* cu_tokens, int num_seqs,
+                      int32_t* matched_pages, int32_t* page_ids, void* stream) {
+  if (!t) return set_err(KVP_EINVAL, "table is NULL");
+  if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
+  if (num_seqs == 0) return KVP_OK;
+  if (!matched_pages) return set_err(KVP_EINVAL, "matched_pages is NULL");
+  Staging::Lease lease;
+  int64_t pages = 0;
+  size_t off = 0;
+  int rc = lease_seq_info(cu_tokens, num_seqs, &lease, &pages, {}, &off);
+  if (rc) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (pages > 0 && (!hashes || !page_ids)) {
+    (void)staging().release(lease, s, false);
+    return set_err(KVP_EINVAL, "hashes or page_ids is NULL");
+  }
+  kvp::TableArgs a{};
+  a.keys = t->keys;
+  a.vals = t->vals;
+  a.mask = t->mask;
+  a.hashes = hashes;
+  a.seq_info = reinterpret_cast<const int4*>(reinterpret_cast<unsigned char*>(lease.host) + off);
+  a.matched = matched_pages;
+  a.out_pages = page_ids;
+  a.err = t->err;
+  hipError_t e = kvp::launch_table(a, 2, num_seqs, s);
+  const int rr = staging().release(lease, s, e == hipSuccess);
+  if (e != hipSuccess) return hip_err(e, "kvp_prefix_lookup launch");
+  return rr;
+}
+
+int kvp_prefix_table_error(kvp_prefix_table_t t, int* code) {
+  if (!t || !code) return set_err(KVP_EINVAL, "table or code is NULL");
+  hipError_t e = hipDeviceSynchronize();
+  int v = 0;
+  if (e == hipSuccess) e = hipMemcpy(&v, t->err, 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemset(t->err, 0, 4);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_err(e, "kvp_prefix_table_error");
+  *code = v;
+  return KVP_OK;
 }
 
 int paged_decode_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int num_seqs,

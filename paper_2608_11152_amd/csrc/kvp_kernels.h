@@ -105,6 +105,35 @@ struct TierArgs {
   int maxp;
 };
 
+// Block hashing: per sequence {first token, full pages, first output slot, 0}.
+struct HashArgs {
+  const int32_t* tokens;
+  const int4* seq_info;     // [num_seqs] (pinned host)
+  uint64_t seed;
+  uint64_t* out;            // [total full pages]
+};
+
+struct GroupLcpArgs {
+  const uint64_t* hashes;
+  const int4* seq_info;     // as in HashArgs
+  const int32_t* grp_off;   // [num_groups + 1] offsets into members (pinned host)
+  const int32_t* members;   // sequence ids of each group's members
+  int32_t* shared_pages;    // [num_groups] device output
+};
+
+struct TableArgs {
+  uint64_t* keys;           // [mask + 1]
+  int32_t* vals;            // [mask + 1]
+  uint64_t mask;
+  const uint64_t* hashes;   // insert / erase: [n]; lookup: per-page hashes laid out as seq_info says
+  const int32_t* pages;     // insert / erase: [n]
+  int64_t n;
+  const int4* seq_info;     // lookup
+  int32_t* matched;         // lookup: [num_seqs]
+  int32_t* out_pages;       // lookup: [total full pages]
+  int* err;
+};
+
 hipError_t launch_append(const AppendArgs& a, int D, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, int D, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
@@ -112,5 +141,9 @@ hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s);
 hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s);
 hipError_t launch_prefill(const PrefillArgs& a, int D, hipStream_t s);
 hipError_t launch_tier(const TierArgs& a, bool restore, hipStream_t s);
+hipError_t launch_block_hash(const HashArgs& a, int n_seqs, hipStream_t s);
+hipError_t launch_group_lcp(const GroupLcpArgs& a, int n_groups, hipStream_t s);
+// op: 0 insert, 1 erase, 2 lookup, 3 clear
+hipError_t launch_table(const TableArgs& a, int op, int n_seqs, hipStream_t s);
 
 }  // namespace kvp

@@ -24,7 +24,9 @@ PAGE = 16
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_reset", "kv_pool_layer_ptr", "kv_pool_info",
            "kv_pool_device_error", "kv_append", "kv_gather", "paged_decode_workspace_size", "paged_decode_attn",
            "prefix_chunk_prefill_workspace_size", "prefix_chunk_prefill_attn", "kv_pool_page_bytes", "kv_offload",
-           "kv_restore", "kvp_check_tables",
+           "kv_restore", "kvp_block_hashes", "kvp_group_shared_pages", "kvp_prefix_table_create",
+           "kvp_prefix_table_destroy", "kvp_prefix_table_clear", "kvp_prefix_table_insert", "kvp_prefix_table_erase",
+           "kvp_prefix_lookup", "kvp_prefix_table_error", "kvp_check_tables",
            "kvp_plan_decode", "kvp_strerror", "kvp_last_error", "kvp_version"]
 
 
@@ -67,6 +69,15 @@ def lib() -> C.CDLL:
         L.kv_pool_page_bytes.argtypes = [p, C.POINTER(sz)]
         L.kv_offload.argtypes = [p, i, i32p, i, vp, vp]
         L.kv_restore.argtypes = [p, i, vp, i32p, i, vp, i, i, i32p, i32p, vp]
+        L.kvp_block_hashes.argtypes = [vp, i32p, i, C.c_uint64, vp, vp]
+        L.kvp_group_shared_pages.argtypes = [vp, i32p, i, i32p, i, vp, vp]
+        L.kvp_prefix_table_create.argtypes = [C.POINTER(p), i]
+        L.kvp_prefix_table_destroy.argtypes = [p]
+        L.kvp_prefix_table_clear.argtypes = [p, vp]
+        L.kvp_prefix_table_insert.argtypes = [p, vp, vp, C.c_int64, vp]
+        L.kvp_prefix_table_erase.argtypes = [p, vp, vp, C.c_int64, vp]
+        L.kvp_prefix_lookup.argtypes = [p, vp, i32p, i, vp, vp, vp]
+        L.kvp_prefix_table_error.argtypes = [p, C.POINTER(i)]
         L.kvp_check_tables.argtypes = [i32p, i, i32p, i, i, gpp]
         L.kvp_plan_decode.argtypes = [i32p, i, gpp, i, i, i32p, i, C.POINTER(i), C.POINTER(i), C.POINTER(i)]
         L.kvp_strerror.argtypes = [i]
@@ -301,6 +312,91 @@ def kv_restore(pool: Pool, layer, host_src, page_ids, block_tables=None, rows=No
         nr, mp, rp, lpp = 0, 0, None, None
     _check(lib().kv_restore(pool.handle, layer, _dptr(host_src), _ptr(ids), len(ids), _dptr(block_tables), nr, mp,
                             rp, lpp, _stream(stream)), "kv_restore")
+
+
+def block_hash_offsets(cu_tokens) -> np.ndarray:
+    """Start of each sequence's block hashes, plus the total, for host cu_tokens (full pages only)."""
+    cu = _i32(cu_tokens)
+    return np.concatenate([[0], np.cumsum(np.diff(cu) // PAGE)]).astype(np.int64)
+
+
+def kvp_block_hashes(tokens, cu_tokens, seed: int = 0, out=None, stream=None):
+    """Block hashes of every full page: tokens device int32; returns device int64 [pages] (uint64 bits)."""
+    import torch
+    cu = _i32(cu_tokens)
+    total = int(block_hash_offsets(cu)[-1])
+    if len(cu) and tokens.numel() < int(cu[-1]):
+        raise ValueError(f"tokens holds {tokens.numel()} ids, cu_tokens ends at {int(cu[-1])}")
+    if out is None:
+        out = torch.empty(max(1, total), dtype=torch.int64, device="cuda")
+    elif out.numel() < total:
+        raise ValueError(f"out holds {out.numel()} hashes, {total} needed")
+    _check(lib().kvp_block_hashes(_dptr(tokens), _ptr(cu), len(cu) - 1, C.c_uint64(seed & (2**64 - 1)), _dptr(out),
+                                  _stream(stream)), "kvp_block_hashes")
+    return out[:total]
+
+
+def kvp_group_shared_pages(hashes, cu_tokens, group_id, num_groups: int, stream=None) -> np.ndarray:
+    """Shared whole pages of each rollout group, derived on the device; returned on the host."""
+    import torch
+    cu, gid = _i32(cu_tokens), _i32(group_id)
+    out = torch.empty(max(1, num_groups), dtype=torch.int32, device="cuda")
+    _check(lib().kvp_group_shared_pages(_dptr(hashes), _ptr(cu), len(cu) - 1, _ptr(gid), num_groups, _dptr(out),
+                                        _stream(stream)), "kvp_group_shared_pages")
+    return out[:num_groups].cpu().numpy()
+
+
+class PrefixTable:
+    """Device hash table from block hash to pool page (kvp_prefix_table_*)."""
+
+    def __init__(self, capacity_log2: int = 20):
+        h = C.c_void_p()
+        _check(lib().kvp_prefix_table_create(C.byref(h), capacity_log2), "kvp_prefix_table_create")
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            lib().kvp_prefix_table_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def clear(self, stream=None):
+        _check(lib().kvp_prefix_table_clear(self.handle, _stream(stream)), "kvp_prefix_table_clear")
+
+    def insert(self, hashes, page_ids, stream=None):
+        if page_ids.numel() < hashes.numel():
+            raise ValueError("one page id per hash")
+        _check(lib().kvp_prefix_table_insert(self.handle, _dptr(hashes), _dptr(page_ids), hashes.numel(),
+                                             _stream(stream)), "kvp_prefix_table_insert")
+
+    def erase(self, hashes, page_ids, stream=None):
+        if page_ids.numel() < hashes.numel():
+            raise ValueError("one page id per hash")
+        _check(lib().kvp_prefix_table_erase(self.handle, _dptr(hashes), _dptr(page_ids), hashes.numel(),
+                                            _stream(stream)), "kvp_prefix_table_erase")
+
+    def lookup(self, hashes, cu_tokens, stream=None):
+        """(matched_pages device int32 [num_seqs], page_ids device int32 [pages])."""
+        import torch
+        cu = _i32(cu_tokens)
+        total = int(block_hash_offsets(cu)[-1])
+        if hashes.numel() < total:
+            raise ValueError(f"hashes holds {hashes.numel()} entries, cu_tokens needs {total}")
+        matched = torch.empty(max(1, len(cu) - 1), dtype=torch.int32, device="cuda")
+        pages = torch.empty(max(1, total), dtype=torch.int32, device="cuda")
+        _check(lib().kvp_prefix_lookup(self.handle, _dptr(hashes), _ptr(cu), len(cu) - 1, _dptr(matched),
+                                       _dptr(pages), _stream(stream)), "kvp_prefix_lookup")
+        return matched[: len(cu) - 1], pages[:total]
+
+    def error(self) -> int:
+        c = C.c_int()
+        _check(lib().kvp_prefix_table_error(self.handle, C.byref(c)), "kvp_prefix_table_error")
+        return c.value
 
 
 def kvp_check_tables(block_tables_host, lens, num_pages, group_prefix=None) -> int:

@@ -390,6 +390,29 @@ def make_values(w: Workload, values: str = "numpy", device=None) -> Values:
     raise ValueError(values)
 
 
+def make_tokens(w: Workload, vocab: int = 151936, lens=None):
+    """Synthetic token ids for every sequence, in position order, drawn per value-table row, so group
+    members carry identical prompt tokens and every other token is independent.  Returns (tokens int32
+    [sum(lens)], cu_tokens int32 [B + 1]) for the first lens[i] tokens of sequence i (default: all)."""
+    rng = np.random.default_rng(w.seed + 104729)
+    ids = rng.integers(0, vocab, size=w.num_token_rows, dtype=np.int64).astype(np.int32)
+    lens = w.final_len if lens is None else np.asarray(lens)
+    parts = [ids[w.token_rows[i][: int(lens[i])]] for i in range(w.B)]
+    cu = np.concatenate([[0], np.cumsum([len(x) for x in parts])]).astype(np.int32)
+    tokens = np.concatenate(parts).astype(np.int32) if parts else np.zeros(0, np.int32)
+    return tokens, cu
+
+
+def step_start(w: Workload) -> np.ndarray:
+    """Tokens each sequence holds before the step's appends (its cached history)."""
+    start = np.asarray(w.final_len, dtype=np.int64).copy()
+    for ab in w.step_appends:
+        for i in range(len(ab.start_pos)):
+            if ab.cu_new[i + 1] > ab.cu_new[i]:
+                start[i] = min(start[i], int(ab.start_pos[i]))
+    return start
+
+
 def seq_kv_bits(w: Workload, vals: Values, i: int, n: int | None = None):
     """Logical (K, V) of sequence i in position order, as raw bf16 bits [n, Hkv, d] (host numpy)."""
     rows = w.token_rows[i][: (w.final_len[i] if n is None else n)]
