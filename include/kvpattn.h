@@ -22,7 +22,8 @@
  *   - Page ids read from device block tables are range-checked on the device.  An id outside
  *     [0, num_pages) is never dereferenced: the kernels skip that page and record KVP_ERANGE in the
  *     pool's device error word, which kv_pool_device_error() returns.
- *   - Only bf16 KV pages and bf16 queries are supported (KVP_BF16); outputs may be bf16 or fp32.
+ *   - Queries are bf16; outputs may be bf16 or fp32.  KV pages are bf16 (KVP_BF16) or OCP FP8 E4M3
+ *     (KVP_FP8_E4M3, one byte per element with a per-layer K scale and V scale, see kv_pool_set_scales).
  *   - page_size is 16 tokens; head_dim is 64 or 128; num_q_heads / num_kv_heads is 1, 2, 4, 8 or 16.
  *
  * Pool layout in HBM (one layer):  bf16 [num_pages][num_kv_heads][2][16 * head_dim]
@@ -33,6 +34,13 @@
  *   where pi(t) swaps bits 2 and 3 of t (an involution: V slots 0..7 hold tokens 0-3 and 8-11, slots
  *   8..15 hold tokens 4-7 and 12-15).  This order makes every operand load of the attention kernels a
  *   16-byte, fully used, contiguous access.  kv_pool_layer_ptr() exposes the raw layer for inspection.
+ *
+ * FP8 pools (KVP_FP8_E4M3): uint8 [num_pages][num_kv_heads][2][16 * head_dim], with byte positions
+ *     K block:  (X * 16 + t) * 16 + ((c / 32) % 2) * 8 + (c % 8),   X = (c / 64) * 4 + (c % 32) / 8
+ *     V block:  ((Y * 2 + s / 8) * 16 + (c % 16)) * 16 + ((c / 16) % 2) * 8 + (s % 8),   Y = c / 32
+ *   (s = pi(t) as above), so one 16-byte load carries the operands of two matrix-core steps.  An element
+ *   x is stored as the E4M3 code of y = fp32(x) * fp32(1 / scale), rounded to nearest with ties to the
+ *   even mantissa and saturated to +-448 (NaN stays NaN); it reads back as code value * scale.
  */
 #ifndef KVPATTN_H
 #define KVPATTN_H
@@ -58,7 +66,7 @@ typedef enum kvp_status {
   KVP_ENOMEM = -8       /* device or pinned-host allocation failed                                   */
 } kvp_status;
 
-typedef enum kvp_dtype { KVP_BF16 = 0, KVP_F32 = 1 } kvp_dtype;
+typedef enum kvp_dtype { KVP_BF16 = 0, KVP_F32 = 1, KVP_FP8_E4M3 = 2 } kvp_dtype;
 
 /* Rollout-group prefix sharing (Sec. 3.1 group id g_r; Sec. 4.4 block-granular reuse).
  *   group_id[i]      host int32 [num_seqs]: group of sequence i, or -1 if ungrouped.
@@ -77,7 +85,7 @@ typedef struct kvp_group_prefix {
  * ------------------------------------------------------------------------------------------------- */
 
 /* Allocate a zero-filled pool of num_layers x num_pages pages on the current HIP device.
- * page_size must be 16, head_dim 64 or 128, dtype KVP_BF16.  *out receives the handle. */
+ * page_size must be 16, head_dim 64 or 128, dtype KVP_BF16 or KVP_FP8_E4M3.  *out receives the handle. */
 int kv_pool_create(kvp_pool_t* out, int num_layers, int num_pages, int page_size, int num_kv_heads,
                    int head_dim, int dtype);
 
@@ -93,6 +101,15 @@ int kv_pool_layer_ptr(kvp_pool_t pool, int layer, void** dev_ptr, size_t* bytes)
 
 /* Pool geometry: any output pointer may be NULL. */
 int kv_pool_info(kvp_pool_t pool, int* num_layers, int* num_pages, int* num_kv_heads, int* head_dim);
+
+/* KV element type of the pool (KVP_BF16 or KVP_FP8_E4M3). */
+int kv_pool_dtype(kvp_pool_t pool, int* dtype);
+
+/* Per-layer quantisation scales of an FP8 pool (both 1.0 when created): K elements are stored as
+ * E4M3(k / k_scale) and V as E4M3(v / v_scale) by kv_append, and read back multiplied by the scale.
+ * Set them before the layer's first append.  Errors: KVP_EINVAL for a scale that is not finite and
+ * positive; KVP_EUNSUPPORTED for a bf16 pool. */
+int kv_pool_set_scales(kvp_pool_t pool, int layer, float k_scale, float v_scale);
 
 /* Synchronise the device, then return (in *code) and clear the first device-side error recorded by
  * kernels using this pool (KVP_OK if none). */
@@ -110,13 +127,15 @@ int kv_pool_device_error(kvp_pool_t pool, int* code);
  *   gp            host, nullable.  When given, a write into any of a member's first shared_pages[g]
  *                 pages is refused with KVP_ESHARED (shared prompt pages are written once, before the
  *                 group is formed, by an append without gp).
- * Errors: KVP_ERANGE if start_pos[i] + count > maxp * 16.  The copy is bit-exact. */
+ * Errors: KVP_ERANGE if start_pos[i] + count > maxp * 16.  The copy is bit-exact (bf16 pools) or the
+ * quantisation defined in the file header (FP8 pools). */
 int kv_append(kvp_pool_t pool, int layer, const void* k, const void* v, const int32_t* block_tables,
               int maxp, const int32_t* start_pos, const int32_t* cu_new, int num_seqs,
               const kvp_group_prefix* gp, void* stream);
 
 /* Read back tokens [0, lens[i]) of every sequence in logical order (inverse of kv_append), for
- * inspection and tests.  k_out, v_out: device bf16 [sum(lens), num_kv_heads, head_dim];
+ * inspection and tests.  k_out, v_out: device bf16 [sum(lens), num_kv_heads, head_dim] (an FP8 pool
+ * returns bf16(fp32(code value) * fp32(scale)), both roundings to nearest even);
  * block_tables device int32 [num_seqs, maxp]; lens host int32 [num_seqs]. */
 int kv_gather(kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp, const int32_t* lens,
               int num_seqs, void* k_out, void* v_out, void* stream);
@@ -175,7 +194,8 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
  * run close to capacity and pages evicted from it come back without recomputation)
  * ------------------------------------------------------------------------------------------------- */
 
-/* Bytes of one pool page of one layer (all KV heads, K and V blocks): num_kv_heads * 64 * head_dim. */
+/* Bytes of one pool page of one layer (all KV heads, K and V blocks): num_kv_heads * 32 * head_dim
+ * bytes per element byte (64 * head_dim * num_kv_heads for bf16, half of that for FP8). */
 int kv_pool_page_bytes(kvp_pool_t pool, size_t* bytes);
 
 /* Copy pool pages page_ids[0 .. n) of `layer` to the host tier: page i goes to host_dst + i * page_bytes,

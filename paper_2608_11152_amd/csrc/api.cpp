@@ -25,6 +25,8 @@ struct kvp_prefix_table {
 
 struct kvp_pool {
   int num_layers = 0, num_pages = 0, num_kv_heads = 0, head_dim = 0, device = 0;
+  int dtype = KVP_BF16;
+  std::vector<float> k_scale, v_scale;  // per layer, FP8 pools
   size_t layer_bytes = 0;
   unsigned char* base = nullptr;  // [layers][pages][Hkv][2][16*d] bf16
   int* err = nullptr;             // device error word
@@ -158,7 +160,11 @@ struct Packer {
 
 bool pool_ok(kvp_pool_t p) { return p && p->base; }
 
-size_t page_bytes(kvp_pool_t p) { return (size_t)p->num_kv_heads * 2 * kvp::kPage * p->head_dim * 2; }
+int elem_bytes(int dtype) { return dtype == KVP_FP8_E4M3 ? 1 : 2; }
+
+size_t page_bytes(kvp_pool_t p) {
+  return (size_t)p->num_kv_heads * 2 * kvp::kPage * p->head_dim * elem_bytes(p->dtype);
+}
 
 // The host tier is read and written by kernels, so it must be pinned host memory (hipHostMalloc, or a
 // torch tensor created with pin_memory=True) that covers `bytes` from `p`.
@@ -344,13 +350,17 @@ int kv_pool_create(kvp_pool_t* out, int num_layers, int num_pages, int page_size
     return set_err(KVP_EINVAL, "num_layers, num_pages and num_kv_heads must be positive");
   if (page_size != kvp::kPage) return set_err(KVP_EUNSUPPORTED, "page_size %d (only 16 is supported)", page_size);
   if (head_dim != 64 && head_dim != 128) return set_err(KVP_EUNSUPPORTED, "head_dim %d (64 or 128)", head_dim);
-  if (dtype != KVP_BF16) return set_err(KVP_EUNSUPPORTED, "dtype %d (only KVP_BF16)", dtype);
+  if (dtype != KVP_BF16 && dtype != KVP_FP8_E4M3)
+    return set_err(KVP_EUNSUPPORTED, "dtype %d (KVP_BF16 or KVP_FP8_E4M3)", dtype);
   auto* p = new kvp_pool();
   p->num_layers = num_layers;
   p->num_pages = num_pages;
   p->num_kv_heads = num_kv_heads;
   p->head_dim = head_dim;
-  p->layer_bytes = (size_t)num_pages * num_kv_heads * 2 * kvp::kPage * head_dim * 2;
+  p->dtype = dtype;
+  p->k_scale.assign(num_layers, 1.0f);
+  p->v_scale.assign(num_layers, 1.0f);
+  p->layer_bytes = (size_t)num_pages * num_kv_heads * 2 * kvp::kPage * head_dim * elem_bytes(dtype);
   hipError_t e = hipGetDevice(&p->device);
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&p->base), p->layer_bytes * num_layers);
   if (e != hipSuccess) {
@@ -403,6 +413,23 @@ int kv_pool_info(kvp_pool_t pool, int* num_layers, int* num_pages, int* num_kv_h
   if (num_pages) *num_pages = pool->num_pages;
   if (num_kv_heads) *num_kv_heads = pool->num_kv_heads;
   if (head_dim) *head_dim = pool->head_dim;
+  return KVP_OK;
+}
+
+int kv_pool_dtype(kvp_pool_t pool, int* dtype) {
+  if (!pool_ok(pool) || !dtype) return set_err(KVP_EINVAL, "pool or dtype is NULL");
+  *dtype = pool->dtype;
+  return KVP_OK;
+}
+
+int kv_pool_set_scales(kvp_pool_t pool, int layer, float k_scale, float v_scale) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (pool->dtype != KVP_FP8_E4M3) return set_err(KVP_EUNSUPPORTED, "scales apply to FP8 pools only");
+  if (!std::isfinite(k_scale) || !(k_scale > 0.0f) || !std::isfinite(v_scale) || !(v_scale > 0.0f))
+    return set_err(KVP_EINVAL, "scales must be finite and > 0");
+  pool->k_scale[layer] = k_scale;
+  pool->v_scale[layer] = v_scale;
   return KVP_OK;
 }
 
@@ -468,6 +495,9 @@ int kv_append(kvp_pool_t pool, int layer, const void* k, const void* v, const in
   a.Hkv = pool->num_kv_heads;
   a.num_pages = pool->num_pages;
   a.err = pool->err;
+  a.fp8 = pool->dtype == KVP_FP8_E4M3;
+  a.inv_scale_k = 1.0f / pool->k_scale[layer];
+  a.inv_scale_v = 1.0f / pool->v_scale[layer];
   hipError_t e = kvp::launch_append(a, pool->head_dim, s);
   (void)hipFreeAsync(druns, s);
   return e == hipSuccess ? KVP_OK : hip_err(e, "kv_append launch");
@@ -508,6 +538,9 @@ int kv_gather(kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
   a.Hkv = pool->num_kv_heads;
   a.num_pages = pool->num_pages;
   a.err = pool->err;
+  a.fp8 = pool->dtype == KVP_FP8_E4M3;
+  a.scale_k = pool->k_scale[layer];
+  a.scale_v = pool->v_scale[layer];
   hipError_t e = kvp::launch_gather(a, pool->head_dim, s);
   (void)hipFreeAsync(druns, s);
   return e == hipSuccess ? KVP_OK : hip_err(e, "kv_gather launch");
@@ -784,6 +817,7 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   if (!q || !out || !block_tables || !seq_lens) return set_err(KVP_EINVAL, "NULL pointer argument");
   if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
   if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
+  if (pool->dtype != KVP_BF16) return set_err(KVP_EUNSUPPORTED, "decode over FP8 pages is not built");
   DecodeLayout L;
   rc = layout_decode(pool, seq_lens, num_seqs, maxp, group_prefix, num_q_heads, &L);
   if (rc) return rc;
@@ -862,6 +896,7 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
   if (!q || !out || !block_tables || !ctx_lens || !cu_q) return set_err(KVP_EINVAL, "NULL pointer argument");
   if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
   if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
+  if (pool->dtype != KVP_BF16) return set_err(KVP_EUNSUPPORTED, "prefill over FP8 pages is not built");
   PrefillLayout L;
   rc = layout_prefill(pool, ctx_lens, cu_q, num_seqs, maxp, num_q_heads, &L);
   if (rc) return rc;

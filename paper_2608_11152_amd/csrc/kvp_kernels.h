@@ -27,6 +27,8 @@ struct AppendArgs {
   int n_runs;
   int maxp, Hkv, num_pages;
   int* err;
+  int fp8;                  // FP8 pool: quantise with the inverse scales
+  float inv_scale_k, inv_scale_v;
 };
 
 struct GatherArgs {
@@ -38,6 +40,8 @@ struct GatherArgs {
   int n_runs;
   int maxp, Hkv, num_pages;
   int* err;
+  int fp8;                  // FP8 pool: dequantise with the scales
+  float scale_k, scale_v;
 };
 
 struct DecodeArgs {

@@ -24,4 +24,18 @@ __host__ __device__ constexpr inline int v_index(int t, int c) {
   return (((c >> 4) * 2 + (s >> 3)) * 16 + (c & 15)) * 8 + (s & 7);
 }
 
+// FP8 (one byte per element) block positions: one 16-byte piece holds the operands of two matrix-core
+// steps.  K piece X = (c/64)*4 + (c%32)/8 of token t carries dims c%8 of step c/32 (even half, then odd).
+// V piece (Y = c/32, slot half s/8, dim c%16) carries slots s%8 of d-tiles 2Y and 2Y+1.
+template <int D>
+__host__ __device__ constexpr inline int k8_index(int t, int c) {
+  return ((((c >> 6) << 2) + ((c & 31) >> 3)) * 16 + t) * 16 + ((c >> 5) & 1) * 8 + (c & 7);
+}
+
+template <int D>
+__host__ __device__ constexpr inline int v8_index(int t, int c) {
+  const int s = slot_token(t);
+  return (((c >> 5) * 2 + (s >> 3)) * 16 + (c & 15)) * 16 + ((c >> 4) & 1) * 8 + (s & 7);
+}
+
 }  // namespace kvp

@@ -17,12 +17,12 @@ LIB_PATH = os.path.join(HERE, "libkvpattn.so")
 
 KVP_OK, KVP_EINVAL, KVP_ERANGE, KVP_EGROUP, KVP_ESHARED, KVP_EWORKSPACE, KVP_EUNSUPPORTED, KVP_EHIP, KVP_ENOMEM = \
     0, -1, -2, -3, -4, -5, -6, -7, -8
-KVP_BF16, KVP_F32 = 0, 1
+KVP_BF16, KVP_F32, KVP_FP8_E4M3 = 0, 1, 2
 PAGE = 16
 
 # Every symbol the header declares (kept in sync by a CPU test that parses include/kvpattn.h).
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_reset", "kv_pool_layer_ptr", "kv_pool_info",
-           "kv_pool_device_error", "kv_append", "kv_gather", "paged_decode_workspace_size", "paged_decode_attn",
+           "kv_pool_dtype", "kv_pool_set_scales", "kv_pool_device_error", "kv_append", "kv_gather", "paged_decode_workspace_size", "paged_decode_attn",
            "prefix_chunk_prefill_workspace_size", "prefix_chunk_prefill_attn", "kv_pool_page_bytes", "kv_offload",
            "kv_restore", "kvp_block_hashes", "kvp_group_shared_pages", "kvp_prefix_table_create",
            "kvp_prefix_table_destroy", "kvp_prefix_table_clear", "kvp_prefix_table_insert", "kvp_prefix_table_erase",
@@ -60,6 +60,8 @@ def lib() -> C.CDLL:
         L.kv_pool_layer_ptr.argtypes = [p, i, C.POINTER(vp), C.POINTER(sz)]
         L.kv_pool_info.argtypes = [p, C.POINTER(i), C.POINTER(i), C.POINTER(i), C.POINTER(i)]
         L.kv_pool_device_error.argtypes = [p, C.POINTER(i)]
+        L.kv_pool_dtype.argtypes = [p, C.POINTER(i)]
+        L.kv_pool_set_scales.argtypes = [p, i, C.c_float, C.c_float]
         L.kv_append.argtypes = [p, i, vp, vp, vp, i, i32p, i32p, i, gpp, vp]
         L.kv_gather.argtypes = [p, i, vp, i, i32p, i, vp, vp, vp]
         L.paged_decode_workspace_size.argtypes = [p, i32p, i, gpp, i, C.POINTER(sz)]
@@ -151,6 +153,25 @@ class Pool:
                "kv_pool_create")
         self.handle = h
         self.num_layers, self.num_pages, self.num_kv_heads, self.head_dim = num_layers, num_pages, num_kv_heads, head_dim
+        self.dtype = dtype
+
+    def set_scales(self, layer: int, k_scale: float, v_scale: float):
+        _check(lib().kv_pool_set_scales(self.handle, layer, float(k_scale), float(v_scale)), "kv_pool_set_scales")
+
+    def kv_dtype(self) -> int:
+        d = C.c_int()
+        _check(lib().kv_pool_dtype(self.handle, C.byref(d)), "kv_pool_dtype")
+        return d.value
+
+    def layer_bytes(self, layer: int = 0):
+        """A zero-copy uint8 device view of one pool layer's raw bytes."""
+        import torch
+        ptr, nbytes = self.layer_ptr(layer)
+
+        class _View:
+            __cuda_array_interface__ = {"shape": (nbytes,), "typestr": "|u1", "data": (ptr, False),
+                                        "version": 3, "strides": None}
+        return torch.as_tensor(_View(), device="cuda")
 
     def close(self):
         if self.handle:

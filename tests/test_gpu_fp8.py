@@ -1,0 +1,101 @@
+"""GPU tests of FP8 (OCP E4M3) KV pools: kv_append's codes bit-exact against the oracle's quantiser in
+the documented byte layout, kv_gather's dequantised values bit-exact, and decode / prefill over FP8
+pages within tolerance of the oracle's attention over the dequantised values."""
+import numpy as np
+import pytest
+
+from gpu_helpers import assert_close, gp_of, note, to_dev_bits
+from oracle import fp8 as F
+from paper_2608_11152_amd import kvpattn as kp
+from paper_2608_11152_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+class Fp8Case:
+    def __init__(self, name, k_scale=1.0, v_scale=1.0, **over):
+        import torch
+        self.w = w = W.make_workload(name, **over)
+        self.vals = W.make_values(w)
+        self.ks, self.vs = k_scale, v_scale
+        self.pool = kp.Pool(1, w.num_pages, w.Hkv, w.d, dtype=kp.KVP_FP8_E4M3)
+        self.pool.set_scales(0, k_scale, v_scale)
+        self.bt = torch.from_numpy(np.ascontiguousarray(w.block_tables)).cuda()
+        kv = to_dev_bits(self.vals.kv)
+        self.gp = gp_of(w)
+        self.ck, self.cv = F.new_pool(w.num_pages, w.Hkv, w.d)
+        for ab in w.setup_appends + w.step_appends:
+            rows = torch.from_numpy(ab.src_rows).cuda()
+            kp.kv_append(self.pool, 0, kv[rows, 0].contiguous(), kv[rows, 1].contiguous(), self.bt, ab.start_pos,
+                         ab.cu_new, group_prefix=self.gp if ab.use_group_prefix else None)
+            x = self.vals.kv[ab.src_rows]
+            F.append(self.ck, self.cv, x[:, 0], x[:, 1], w.block_tables, ab.start_pos, ab.cu_new, k_scale, v_scale)
+        torch.cuda.synchronize()
+
+
+def _k_pos(t, c):
+    return (((c // 64) * 4 + (c % 32) // 8) * 16 + t) * 16 + ((c // 32) % 2) * 8 + c % 8
+
+
+def _v_pos(t, c, D):
+    s = (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1)
+    return 16 * D + ((((c // 32) * 2 + s // 8) * 16 + c % 16) * 16 + ((c // 16) % 2) * 8 + s % 8)
+
+
+@pytest.mark.parametrize("name,ks,vs", [("tiny", 1.0, 1.0), ("mixed_s", 0.37, 1.9), ("rlvr_d64", 0.5, 0.5)])
+def test_fp8_append_codes_in_documented_layout(name, ks, vs):
+    note(f"fp8 append layout {name} scales {ks} {vs}")
+    c = Fp8Case(name, ks, vs)
+    w = c.w
+    raw = c.pool.layer_bytes(0).cpu().numpy().reshape(w.num_pages, w.Hkv, 2 * 16 * w.d)
+    t = np.arange(16)[:, None]
+    cc = np.arange(w.d)[None, :]
+    ik, iv = _k_pos(t, cc), _v_pos(t, cc, w.d)
+    pages = np.unique(w.block_tables[w.block_tables >= 0])
+    for page in pages:
+        for h in range(w.Hkv):
+            assert np.array_equal(raw[page, h][ik], c.ck[page, h]), ("K", page, h)
+            assert np.array_equal(raw[page, h][iv], c.cv[page, h]), ("V", page, h)
+    assert c.pool.device_error() == kp.KVP_OK
+
+
+@pytest.mark.parametrize("name,ks,vs", [("mixed_s", 0.37, 1.9), ("rlvr_d64", 1.0, 1.0)])
+def test_fp8_gather_dequantised_bitexact(name, ks, vs):
+    import torch
+    note(f"fp8 gather {name}")
+    c = Fp8Case(name, ks, vs)
+    w = c.w
+    k, v = kp.kv_gather(c.pool, 0, c.bt, w.final_len)
+    torch.cuda.synchronize()
+    kb = k.view(torch.int16).cpu().numpy().view(np.uint16)
+    vb = v.view(torch.int16).cpu().numpy().view(np.uint16)
+    off = 0
+    for i in range(w.B):
+        n = int(w.final_len[i])
+        pos = np.arange(n)
+        pg = w.block_tables[i][pos // 16]
+        ek = F.dequantize_bf16(c.ck[pg, :, pos % 16, :], ks)
+        ev = F.dequantize_bf16(c.cv[pg, :, pos % 16, :], vs)
+        assert np.array_equal(kb[off:off + n], ek), f"K of sequence {i}"
+        assert np.array_equal(vb[off:off + n], ev), f"V of sequence {i}"
+        off += n
+
+
+def test_fp8_pool_settings():
+    pool = kp.Pool(2, 16, 2, 64, dtype=kp.KVP_FP8_E4M3)
+    assert pool.kv_dtype() == kp.KVP_FP8_E4M3
+    assert kp.kv_pool_page_bytes(pool) == 2 * 2 * 16 * 64
+    _, nbytes = pool.layer_ptr(1)
+    assert nbytes == 16 * 2 * 2 * 16 * 64
+    for bad in ((0.0, 1.0), (1.0, -1.0), (float("inf"), 1.0), (float("nan"), 1.0)):
+        with pytest.raises(kp.KvpError) as ei:
+            pool.set_scales(0, *bad)
+        assert ei.value.code == kp.KVP_EINVAL
+    with pytest.raises(kp.KvpError) as ei:
+        pool.set_scales(2, 1.0, 1.0)
+    assert ei.value.code == kp.KVP_EINVAL
+    bf = kp.Pool(1, 16, 2, 64)
+    assert bf.kv_dtype() == kp.KVP_BF16
+    with pytest.raises(kp.KvpError) as ei:
+        bf.set_scales(0, 1.0, 1.0)
+    assert ei.value.code == kp.KVP_EUNSUPPORTED
