@@ -817,7 +817,6 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   if (!q || !out || !block_tables || !seq_lens) return set_err(KVP_EINVAL, "NULL pointer argument");
   if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
   if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
-  if (pool->dtype != KVP_BF16) return set_err(KVP_EUNSUPPORTED, "decode over FP8 pages is not built");
   DecodeLayout L;
   rc = layout_decode(pool, seq_lens, num_seqs, maxp, group_prefix, num_q_heads, &L);
   if (rc) return rc;
@@ -849,7 +848,9 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   a.Hkv = pool->num_kv_heads;
   a.G = num_q_heads / pool->num_kv_heads;
   a.num_pages = pool->num_pages;
-  a.scale_log2 = scale * 1.4426950408889634f;
+  a.fp8 = pool->dtype == KVP_FP8_E4M3;
+  a.scale_log2 = scale * 1.4426950408889634f * (a.fp8 ? pool->k_scale[layer] : 1.0f);
+  a.v_scale = a.fp8 ? pool->v_scale[layer] : 1.0f;
   a.err = pool->err;
   a.items = reinterpret_cast<const kvp::DecodeItem*>(m + L.off_wave);
   a.seg_off = reinterpret_cast<const int32_t*>(m + L.off_seg);

@@ -120,7 +120,7 @@ template <int D, int NT>
 __device__ __forceinline__ void write_state(const DecodeArgs& a, const DecodeItem& it, const SoftState<NT>& st,
                                             int seq, int head, int q4) {
   if (it.slot < 0) {
-    const float inv = st.l > 0.0f ? 1.0f / st.l : 0.0f;
+    const float inv = st.l > 0.0f ? a.v_scale / st.l : 0.0f;
     const int64_t o = ((int64_t)seq * a.Hq + head) * D + 4 * q4;
 #pragma unroll
     for (int d = 0; d < NT; ++d) {
@@ -138,7 +138,7 @@ __device__ __forceinline__ void write_state(const DecodeArgs& a, const DecodeIte
     const int64_t pidx = (int64_t)a.part_base[seq] + it.slot;
     float* pa = a.part_acc + (pidx * a.Hq + head) * D + 4 * q4;
 #pragma unroll
-    for (int d = 0; d < NT; ++d) *reinterpret_cast<f32x4*>(pa + 16 * d) = st.acc[d];
+    for (int d = 0; d < NT; ++d) *reinterpret_cast<f32x4*>(pa + 16 * d) = st.acc[d] * a.v_scale;
     if (q4 == 0) a.part_ml[pidx * a.Hq + head] = make_float2(st.m, st.l);
   }
 }
@@ -216,23 +216,6 @@ __device__ __forceinline__ void decode_wave_chunk(const DecodeArgs& a, const Dec
   st.l += __shfl_xor(st.l, 16);
   st.l += __shfl_xor(st.l, 32);
   if (col_ok) write_state<D, NT>(a, it, st, seq, head, q4);
-}
-
-// ---------------------------------------------------------------------------------------------------
-// Wave path: private page ranges, and shared-prefix ranges of groups with <= 16 query columns.  The
-// planner cuts the concatenated page ranges into equal segments; waves s*Hkv .. s*Hkv+Hkv-1 process
-// segment s, one KV head each, chunk after chunk.  Operands are loaded straight from HBM; each
-// two-page step issues 2*D/32 K loads and D/16 V loads of 16 bytes per lane (16 KB per wave, d = 128).
-// ---------------------------------------------------------------------------------------------------
-template <int D>
-__device__ __forceinline__ void decode_wave_block(const DecodeArgs& a, int block) {
-  const int lane = threadIdx.x & 63;
-  const int wid = block * 4 + (threadIdx.x >> 6);
-  const int seg = wid / a.Hkv;
-  const int kvh = wid - seg * a.Hkv;
-  if (seg >= a.n_items) return;
-  const int c1 = a.seg_off[seg + 1];
-  for (int c = a.seg_off[seg]; c < c1; ++c) decode_wave_chunk<D>(a, a.items[c], kvh, lane);
 }
 
 // ---------------------------------------------------------------------------------------------------
@@ -366,17 +349,284 @@ __device__ __forceinline__ void decode_group_block(const DecodeArgs& a, int bloc
 }
 
 // ---------------------------------------------------------------------------------------------------
+// FP8 (E4M3) pages.  One 16-byte piece of a page block carries the operands of two matrix-core steps
+// (kvp_layout.h), converted exactly to bf16 in registers; the K scale is folded into the score scale and
+// the V scale into the output.  A step covers four pages (16 KB of K and V per wave, as the bf16 path
+// moves per two pages) and computes them as two two-page sub-steps.
+// ---------------------------------------------------------------------------------------------------
+__device__ __forceinline__ unsigned cvt_fp8x2(unsigned w, bool hi) {
+  return __builtin_bit_cast(unsigned, hi ? __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, true)
+                                         : __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false));
+}
+
+// 16 codes -> the bf16 operand of bytes 0-7 (lo) and of bytes 8-15 (hi).
+__device__ __forceinline__ void cvt_piece(u32x4 r, u32x4& lo, u32x4& hi) {
+  lo = u32x4{cvt_fp8x2(r[0], false), cvt_fp8x2(r[0], true), cvt_fp8x2(r[1], false), cvt_fp8x2(r[1], true)};
+  hi = u32x4{cvt_fp8x2(r[2], false), cvt_fp8x2(r[2], true), cvt_fp8x2(r[3], false), cvt_fp8x2(r[3], true)};
+}
+
+// Scores and PV of one two-page sub-step from raw K / V pieces (NS/2 K pieces per score tile, NT/2 V
+// pieces), for pages whose validity the caller has resolved.
+template <int NS, int NT>
+__device__ __forceinline__ void fp8_substep(SoftState<NT>& st, const u32x4 (&qt)[NS], const u32x4 (&kxr)[NS / 2],
+                                            const u32x4 (&kyr)[NS / 2], const u32x4 (&vr)[NT / 2], float scale_log2,
+                                            const bool (&ok)[8], bool masked) {
+  f32x4 sx = {0.f, 0.f, 0.f, 0.f}, sy = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int p2 = 0; p2 < NS / 2; ++p2) {
+    u32x4 a0, a1, b0, b1;
+    cvt_piece(kxr[p2], a0, a1);
+    cvt_piece(kyr[p2], b0, b1);
+    sx = mfma16(a0, qt[2 * p2], sx);
+    sy = mfma16(b0, qt[2 * p2], sy);
+    sx = mfma16(a1, qt[2 * p2 + 1], sx);
+    sy = mfma16(b1, qt[2 * p2 + 1], sy);
+  }
+  u32x4 vv[NT];
+#pragma unroll
+  for (int y = 0; y < NT / 2; ++y) cvt_piece(vr[y], vv[2 * y], vv[2 * y + 1]);
+  softmax_pv<NT>(st, sx, sy, scale_log2, ok, masked, vv);
+}
+
+template <int D>
+__device__ __forceinline__ void decode_wave_chunk_fp8(const DecodeArgs& a, const DecodeItem& it, int kvh, int lane) {
+  constexpr int NS = D / 32;
+  constexpr int NT = D / 16;
+  constexpr int KB = 16 * D;  // bytes per K (or V) block
+  const int q4 = lane >> 4, c16 = lane & 15;
+  const int ncols = it.n_mem * a.G;
+  const bool col_ok = c16 < ncols;
+  int seq = 0, head = 0;
+  if (col_ok) {
+    const int m = c16 / a.G;
+    seq = a.members[it.mem_off + m];
+    head = kvh * a.G + (c16 - m * a.G);
+  }
+  u32x4 qt[NS];
+  {
+    const uint16_t* qr = a.q + ((int64_t)seq * a.Hq + head) * D;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qt[s] = col_ok ? ld16(qr + 8 * (4 * s + q4)) : u32x4{0u, 0u, 0u, 0u};
+  }
+  SoftState<NT> st;
+#pragma unroll
+  for (int d = 0; d < NT; ++d) st.acc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  st.m = -INFINITY;
+  st.l = 0.f;
+
+  const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
+  const unsigned char* hbase = reinterpret_cast<const unsigned char*>(a.layer) + (int64_t)kvh * 2 * KB;
+  const int32_t* btr = a.bt + (int64_t)it.row * a.maxp;
+  const int k_off = ((q4)*16 + (c16 & 7)) * 16;                       // + p2 * 1024 (4 chunks of 256 B)
+  const int v_off = KB + (((q4 & 1)) * 16 + c16) * 16;                // + y * 512
+  bool bad = false;
+  for (int p = it.page_lo; p < it.page_hi; p += 4) {
+    int id[4];
+    bool val[4], has[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      has[j] = p + j < it.page_hi;
+      id[j] = has[j] ? btr[p + j] : 0;
+      val[j] = has[j] && (unsigned)id[j] < (unsigned)a.num_pages;
+      bad |= has[j] && !val[j];
+      if (!val[j]) id[j] = 0;
+    }
+    const bool two = has[2];
+    u32x4 kxr[2][NS / 2], kyr[2][NS / 2], vr[2][NT / 2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (u == 1 && !two) break;
+      const unsigned char* px = hbase + (int64_t)id[2 * u] * page_stride;
+      const unsigned char* py = hbase + (int64_t)(has[2 * u + 1] ? id[2 * u + 1] : id[2 * u]) * page_stride;
+      const unsigned char* kp = (c16 < 8 ? px : py) + k_off;
+      const unsigned char* vp = (q4 < 2 ? px : py) + v_off;
+#pragma unroll
+      for (int p2 = 0; p2 < NS / 2; ++p2) {
+        kxr[u][p2] = ld16_stream(kp + p2 * 1024);
+        kyr[u][p2] = ld16_stream(kp + p2 * 1024 + 128);
+      }
+#pragma unroll
+      for (int y = 0; y < NT / 2; ++y) vr[u][y] = ld16_stream(vp + y * 512);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (u == 1 && !two) break;
+      const int x = p + 2 * u;
+      const bool hb = has[2 * u + 1];
+      const bool va = val[2 * u], vb = hb && val[2 * u + 1];
+      const bool masked = !hb || !va || !vb || (x + 2) * 16 > it.tok_end;
+      bool ok[8];
+      lane_token_ok(x, q4, q4 < 2 ? va : vb, it.tok_end, ok);
+      fp8_substep<NS, NT>(st, qt, kxr[u], kyr[u], vr[u], a.scale_log2, ok, masked);
+    }
+  }
+  if (bad && lane == 0) atomicCAS(a.err, 0, KVP_ERANGE);
+  st.l += __shfl_xor(st.l, 16);
+  st.l += __shfl_xor(st.l, 32);
+  if (col_ok) write_state<D, NT>(a, it, st, seq, head, q4);
+}
+
+template <int D>
+struct GroupLds8 {
+  static constexpr int KB = 16 * D;      // bytes per K (or V) block
+  static constexpr int PB = 2 * KB;      // bytes per (page, head): K + V blocks
+  static constexpr int PAD = 128;        // keeps consecutive staged pages on different LDS banks
+  static constexpr int SB = 4 * (PB + PAD);
+  static constexpr int bytes = 2 * SB;   // double-buffered four-page stage
+};
+
+template <int D>
+__device__ __forceinline__ void decode_group_block_fp8(const DecodeArgs& a, int block, unsigned char* lds) {
+  constexpr int NS = D / 32;
+  constexpr int NT = D / 16;
+  constexpr int KB = GroupLds8<D>::KB;
+  constexpr int PB = GroupLds8<D>::PB;
+  constexpr int PAD = GroupLds8<D>::PAD;
+  constexpr int SB = GroupLds8<D>::SB;
+  constexpr int NCH = 4 * PB / (256 * 16);
+
+  const int item = block / a.Hkv;
+  const int kvh = block - item * a.Hkv;
+  if (item >= a.n_group_items) return;
+  const DecodeItem it = a.group_items[item];
+  const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, q4 = lane >> 4, c16 = lane & 15;
+  const int ncols = it.n_mem * a.G;
+  const int col = wv * 16 + c16;
+  const bool wave_on = wv * 16 < ncols;
+  const bool col_ok = col < ncols;
+  int seq = 0, head = 0;
+  if (col_ok) {
+    const int m = col / a.G;
+    seq = a.members[it.mem_off + m];
+    head = kvh * a.G + (col - m * a.G);
+  }
+  u32x4 qt[NS];
+  {
+    const uint16_t* qr = a.q + ((int64_t)seq * a.Hq + head) * D;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qt[s] = col_ok ? ld16(qr + 8 * (4 * s + q4)) : u32x4{0u, 0u, 0u, 0u};
+  }
+  SoftState<NT> st;
+#pragma unroll
+  for (int d = 0; d < NT; ++d) st.acc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  st.m = -INFINITY;
+  st.l = 0.f;
+
+  const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
+  const unsigned char* hbase = reinterpret_cast<const unsigned char*>(a.layer) + (int64_t)kvh * 2 * KB;
+  const int32_t* btr = a.bt + (int64_t)it.row * a.maxp;
+  bool bad = false;
+
+  // Stage pages p..p+3 into registers; pages past the range or with invalid ids become zeros.
+  auto fetch = [&](int p, u32x4 (&r)[NCH]) {
+    int id[4];
+    bool okp[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool has = p + j < it.page_hi;
+      id[j] = has ? btr[p + j] : 0;
+      okp[j] = has && (unsigned)id[j] < (unsigned)a.num_pages;
+      bad |= has && !okp[j];
+    }
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      const int off = (k * 256 + tid) * 16;
+      const int pg = off / PB, inb = off - pg * PB;
+      r[k] = okp[pg] ? ld16_stream(hbase + (int64_t)id[pg] * page_stride + inb) : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto store = [&](int buf, const u32x4 (&r)[NCH]) {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      const int off = (k * 256 + tid) * 16;
+      const int pg = off / PB, inb = off - pg * PB;
+      *reinterpret_cast<u32x4*>(lds + buf * SB + pg * (PB + PAD) + inb) = r[k];
+    }
+  };
+
+  u32x4 r[NCH];
+  fetch(it.page_lo, r);
+  store(0, r);
+  __syncthreads();
+  int buf = 0;
+  for (int p = it.page_lo; p < it.page_hi; p += 4) {
+    const bool more = p + 4 < it.page_hi;
+    if (more) fetch(p + 4, r);
+    if (wave_on) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int x = p + 2 * u;
+        if (x >= it.page_hi) break;
+        const unsigned char* sx0 = lds + buf * SB + (2 * u) * (PB + PAD);
+        const unsigned char* sy0 = sx0 + (PB + PAD);
+        const unsigned char* kp = (c16 < 8 ? sx0 : sy0) + (q4 * 16 + (c16 & 7)) * 16;
+        const unsigned char* vp = (q4 < 2 ? sx0 : sy0) + KB + ((q4 & 1) * 16 + c16) * 16;
+        u32x4 kxr[NS / 2], kyr[NS / 2], vr[NT / 2];
+#pragma unroll
+        for (int p2 = 0; p2 < NS / 2; ++p2) {
+          kxr[p2] = ld16(kp + p2 * 1024);
+          kyr[p2] = ld16(kp + p2 * 1024 + 128);
+        }
+#pragma unroll
+        for (int y = 0; y < NT / 2; ++y) vr[y] = ld16(vp + y * 512);
+        const bool hb = x + 1 < it.page_hi;
+        const bool va = (unsigned)btr[x] < (unsigned)a.num_pages;
+        const bool vb = hb && (unsigned)btr[x + 1] < (unsigned)a.num_pages;
+        const bool masked = !hb || !va || !vb || (x + 2) * 16 > it.tok_end;
+        bool ok[8];
+        lane_token_ok(x, q4, q4 < 2 ? va : vb, it.tok_end, ok);
+        fp8_substep<NS, NT>(st, qt, kxr, kyr, vr, a.scale_log2, ok, masked);
+      }
+    }
+    if (more) store(buf ^ 1, r);
+    __syncthreads();
+    buf ^= 1;
+  }
+  if (bad && tid == 0) atomicCAS(a.err, 0, KVP_ERANGE);
+  if (!wave_on) return;
+  st.l += __shfl_xor(st.l, 16);
+  st.l += __shfl_xor(st.l, 32);
+  if (!col_ok) return;
+  write_state<D, NT>(a, it, st, seq, head, q4);
+}
+
+// ---------------------------------------------------------------------------------------------------
+// Wave path: private page ranges, and shared-prefix ranges of groups with <= 16 query columns.  The
+// planner cuts the concatenated page ranges into equal segments; waves s*Hkv .. s*Hkv+Hkv-1 process
+// segment s, one KV head each, chunk after chunk.  Operands are loaded straight from HBM; each
+// two-page step issues 2*D/32 K loads and D/16 V loads of 16 bytes per lane (16 KB per wave, d = 128).
+// ---------------------------------------------------------------------------------------------------
+template <int D, bool FP8>
+__device__ __forceinline__ void decode_wave_block(const DecodeArgs& a, int block) {
+  const int lane = threadIdx.x & 63;
+  const int wid = block * 4 + (threadIdx.x >> 6);
+  const int seg = wid / a.Hkv;
+  const int kvh = wid - seg * a.Hkv;
+  if (seg >= a.n_items) return;
+  const int c1 = a.seg_off[seg + 1];
+  for (int c = a.seg_off[seg]; c < c1; ++c) {
+    if constexpr (FP8) decode_wave_chunk_fp8<D>(a, a.items[c], kvh, lane);
+    else decode_wave_chunk<D>(a, a.items[c], kvh, lane);
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------
 // One launch for both paths: blocks [0, n_wave_blocks) run 4 wave-path waves each; the remaining
 // blocks run the LDS-staged shared-prefix path, one per (prefix item, KV head).  Blocks are dispatched
 // in index order, so the wave blocks take the first round and the shared-prefix blocks run in the
 // slots the planner left free for them.  The two paths need the same number of registers to within a
 // few, so sharing a launch costs no occupancy and saves a launch boundary.
 // ---------------------------------------------------------------------------------------------------
-template <int D>
+template <int D, bool FP8>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
-  __shared__ __attribute__((aligned(16))) unsigned char lds[GroupLds<D>::bytes];
-  if ((int)blockIdx.x < a.n_wave_blocks) decode_wave_block<D>(a, blockIdx.x);
-  else decode_group_block<D>(a, (int)blockIdx.x - a.n_wave_blocks, lds);
+  constexpr int LB = FP8 ? GroupLds8<D>::bytes : GroupLds<D>::bytes;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LB];
+  if ((int)blockIdx.x < a.n_wave_blocks) {
+    decode_wave_block<D, FP8>(a, blockIdx.x);
+  } else {
+    if constexpr (FP8) decode_group_block_fp8<D>(a, (int)blockIdx.x - a.n_wave_blocks, lds);
+    else decode_group_block<D>(a, (int)blockIdx.x - a.n_wave_blocks, lds);
+  }
 }
 
 // ---------------------------------------------------------------------------------------------------
@@ -483,8 +733,15 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
 hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s) {
   const int64_t blocks = (int64_t)a.n_wave_blocks + a.n_group_blocks;
   if (blocks == 0) return hipSuccess;
-  if (D == 128) hipLaunchKernelGGL(decode_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(decode_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)blocks);
+  if (a.fp8) {
+    if (D == 128) hipLaunchKernelGGL((decode_kernel<128, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((decode_kernel<64, true>), grid, dim3(256), 0, s, a);
+  } else if (D == 128) {
+    hipLaunchKernelGGL((decode_kernel<128, false>), grid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((decode_kernel<64, false>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -63,7 +63,9 @@ struct DecodeArgs {
   void* out;                // [B, Hq, D]
   int out_f32;
   int Hq, Hkv, G, num_pages;
-  float scale_log2;         // scale * log2(e)
+  float scale_log2;         // scale * log2(e) (times the K scale of an FP8 pool)
+  float v_scale;            // 1, or the V scale of an FP8 pool (applied to the output)
+  int fp8;                  // pages are FP8 E4M3
   int* err;
 };
 

@@ -99,3 +99,37 @@ def test_fp8_pool_settings():
     with pytest.raises(kp.KvpError) as ei:
         bf.set_scales(0, 1.0, 1.0)
     assert ei.value.code == kp.KVP_EUNSUPPORTED
+
+
+def _decode(c, gp="auto", out_dtype=None):
+    import torch
+    w = c.w
+    q = to_dev_bits(c.vals.q)
+    out = kp.paged_decode_attn(q, c.pool, 0, c.bt, w.decode_len, group_prefix=c.gp if gp == "auto" else gp,
+                               scale=w.scale, out_dtype=out_dtype or torch.float32)
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("name,ks,vs", [("tiny", 1.0, 1.0), ("rlvr_s", 0.37, 1.9), ("rlhf_s", 1.0, 1.0),
+                                         ("agentic_s", 0.5, 2.0), ("mixed_s", 1.0, 0.8), ("rlvr_d64", 1.3, 0.6)])
+def test_fp8_decode_parity(name, ks, vs):
+    note(f"fp8 decode {name} scales {ks} {vs}")
+    c = Fp8Case(name, ks, vs)
+    w = c.w
+    ref = F.decode(c.vals.q, c.ck, c.cv, w.block_tables, w.decode_len, w.scale, ks, vs)
+    assert_close(_decode(c), ref, f"fp8 decode {name}")
+    if c.gp is not None:
+        assert_close(_decode(c, gp=None), ref, f"fp8 decode {name} without the group hint")
+    assert c.pool.device_error() == kp.KVP_OK
+
+
+def test_fp8_decode_bf16_out_and_determinism():
+    import torch
+    c = Fp8Case("mixed_s", 0.7, 1.1)
+    note("fp8 decode bf16 out, determinism")
+    a = _decode(c, out_dtype=torch.bfloat16)
+    b = _decode(c, out_dtype=torch.bfloat16)
+    assert torch.equal(a, b)
+    ref = F.decode(c.vals.q, c.ck, c.cv, c.w.block_tables, c.w.decode_len, c.w.scale, 0.7, 1.1)
+    assert_close(a, ref, "fp8 decode bf16 out")
