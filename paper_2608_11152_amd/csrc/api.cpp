@@ -897,7 +897,6 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
   if (!q || !out || !block_tables || !ctx_lens || !cu_q) return set_err(KVP_EINVAL, "NULL pointer argument");
   if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
   if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
-  if (pool->dtype != KVP_BF16) return set_err(KVP_EUNSUPPORTED, "prefill over FP8 pages is not built");
   PrefillLayout L;
   rc = layout_prefill(pool, ctx_lens, cu_q, num_seqs, maxp, num_q_heads, &L);
   if (rc) return rc;
@@ -923,7 +922,9 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
   a.Hkv = pool->num_kv_heads;
   a.G = num_q_heads / pool->num_kv_heads;
   a.num_pages = pool->num_pages;
-  a.scale_log2 = scale * 1.4426950408889634f;
+  a.fp8 = pool->dtype == KVP_FP8_E4M3;
+  a.scale_log2 = scale * 1.4426950408889634f * (a.fp8 ? pool->k_scale[layer] : 1.0f);
+  a.v_scale = a.fp8 ? pool->v_scale[layer] : 1.0f;
   a.err = pool->err;
   hipError_t e = kvp::launch_prefill(a, pool->head_dim, s);
   return e == hipSuccess ? KVP_OK : hip_err(e, "prefix_chunk_prefill_attn launch");

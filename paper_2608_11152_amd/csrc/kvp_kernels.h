@@ -91,7 +91,9 @@ struct PrefillArgs {
   void* out;
   int out_f32;
   int Hq, Hkv, G, num_pages;
-  float scale_log2;
+  float scale_log2;         // scale * log2(e) (times the K scale of an FP8 pool)
+  float v_scale;            // 1, or the V scale of an FP8 pool
+  int fp8;
   int* err;
 };
 

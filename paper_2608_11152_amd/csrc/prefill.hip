@@ -35,12 +35,25 @@ __device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <int D>
+// FP8 pages (FP8 = true): a stage holds half the bytes; every 16-byte K piece read from LDS carries the
+// operands of two k-steps and every V operand is an 8-byte read, both converted exactly to bf16 in
+// registers.  The K scale is folded into the score scale and the V scale into the output.
+__device__ __forceinline__ unsigned cvt_fp8x2(unsigned w, bool hi) {
+  return __builtin_bit_cast(unsigned, hi ? __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, true)
+                                         : __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false));
+}
+
+__device__ __forceinline__ u32x4 cvt8(unsigned w0, unsigned w1) {
+  return u32x4{cvt_fp8x2(w0, false), cvt_fp8x2(w0, true), cvt_fp8x2(w1, false), cvt_fp8x2(w1, true)};
+}
+
+template <int D, bool FP8>
 __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   constexpr int NS = D / 16;           // k-steps of the score product
   constexpr int NDT = D / 32;          // 32-row d tiles of the output
   constexpr int KB = 16 * D;           // elements per K (or V) block
-  constexpr int PB = 4 * KB;           // bytes per (page, head) block
+  constexpr int KBB = FP8 ? KB : 2 * KB;  // bytes per K (or V) block
+  constexpr int PB = 2 * KBB;          // bytes per (page, head) block
   constexpr int NPG = 4;               // pages per stage
   constexpr int SB = NPG * PB;
   constexpr int NCH = SB / (256 * 16);
@@ -49,6 +62,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   const PrefillItem it = a.items[blockIdx.x];
   if (it.seq < 0) return;
   const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
+  const int wvu = __builtin_amdgcn_readfirstlane(wv);  // the same value, known to be wave-uniform
   const int G = a.G;
   const int ctx = a.ctx_lens[it.seq];
   const int q0 = a.cu_q[it.seq];
@@ -76,8 +90,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   float m_run = -INFINITY, l_run = 0.0f;
   const float cs = a.scale_log2;
 
-  const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
-  const uint16_t* hbase = a.layer + (int64_t)it.kvh * 2 * KB;
+  const int64_t page_stride = (int64_t)a.Hkv * PB;  // bytes
+  const unsigned char* hbase = reinterpret_cast<const unsigned char*>(a.layer) + (int64_t)it.kvh * PB;
   // The block table is read-only for the kernel's lifetime: read it through the constant address space
   // so page ids are scalar loads (counted apart from the LDS copies, which the compiler must not wait on).
   typedef const __attribute__((address_space(4))) int32_t* const_i32p;
@@ -101,14 +115,25 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       const bool inr = st * NPG + pg < n_pages;
       okp[pg] = inr && (unsigned)ids[pg] < (unsigned)a.num_pages;
       bad |= inr && !okp[pg];
-      const int id = okp[pg] ? ids[pg] : 0;
-      const unsigned char* src = reinterpret_cast<const unsigned char*>(hbase + (int64_t)id * page_stride) + tid * 16;
+      ids[pg] = okp[pg] ? ids[pg] : 0;
+      if constexpr (CPP >= 1) {
+        const unsigned char* src = hbase + (int64_t)ids[pg] * page_stride + tid * 16;
 #pragma unroll
-      for (int c = 0; c < CPP; ++c) {
-        const int k = pg * CPP + c;
-        __builtin_amdgcn_global_load_lds(src + c * (256 * 16),
-                                         (__attribute__((address_space(3))) void*)(lds + buf * SB + k * 4096 + wv * 1024),
-                                         16, 0, 0);
+        for (int c = 0; c < CPP; ++c) {
+          const int k = pg * CPP + c;
+          __builtin_amdgcn_global_load_lds(src + c * (256 * 16),
+                                           (__attribute__((address_space(3))) void*)(lds + buf * SB + k * 4096 + wv * 1024),
+                                           16, 0, 0);
+        }
+      }
+    }
+    if constexpr (CPP == 0) {
+      // A page block is smaller than one copy round: round k's wave pieces span 4096 / PB pages.
+#pragma unroll
+      for (int k = 0; k < NCH; ++k) {
+        const int o = k * 4096 + wvu * 1024;
+        const unsigned char* src = hbase + (int64_t)ids[o / PB] * page_stride + (o % PB) + lane * 16;
+        __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(lds + buf * SB + o), 16, 0, 0);
       }
     }
   };
@@ -117,24 +142,35 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) any |= !okp[pg];
     if (!any) return;
+    // Piece k of this thread: stage bytes [4096k + 16 tid, +16), in page (4096k + 1024 wv) / PB.
 #pragma unroll
-    for (int pg = 0; pg < NPG; ++pg) {
+    for (int k = 0; k < NCH; ++k) {
+      const int o = k * 4096 + wvu * 1024;
+      const int pg = o / PB;
       const int valid = okp[pg] ? seq_tokens - (st * NPG + pg) * 16 : 0;  // usable tokens of this page
       if (valid >= 16) continue;
-#pragma unroll
-      for (int c = 0; c < CPP; ++c) {
-        const int inb = c * (256 * 16) + tid * 16;
-        u32x4* lp = reinterpret_cast<u32x4*>(lds + buf * SB + ((pg * CPP + c) * 256 + tid) * 16);
+      {
+        const int inb = (o % PB) + lane * 16;
+        u32x4* lp = reinterpret_cast<u32x4*>(lds + buf * SB + o + lane * 16);
         u32x4 v = *lp;
-        if (inb < 2 * KB) {
+        if (inb < KBB) {
           if (((inb >> 4) & 15) >= valid) v = u32x4{0u, 0u, 0u, 0u};
-        } else {
-          const int h = ((inb - 2 * KB) >> 8) & 1;  // V chunk holds slots 8h..8h+7
+        } else if (!FP8) {
+          const int h = ((inb - KBB) >> 8) & 1;  // V chunk holds slots 8h..8h+7
 #pragma unroll
           for (int w = 0; w < 4; ++w) {
             const unsigned lo = slot_token(8 * h + 2 * w) < valid ? 0xFFFFu : 0u;
             const unsigned hi = slot_token(8 * h + 2 * w + 1) < valid ? 0xFFFF0000u : 0u;
             v[w] &= lo | hi;
+          }
+        } else {
+          const int h = ((inb - KBB) >> 8) & 1;  // V piece holds slots 8h..8h+7 of two d-tiles
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            unsigned m = 0u;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) m |= (slot_token(8 * h + ((4 * w + b) & 7)) < valid ? 0xFFu : 0u) << (8 * b);
+            v[w] &= m;
           }
         }
         *lp = v;
@@ -158,11 +194,27 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // MFMA chains are interleaved; the V fragments are read next so their latency hides behind the
     // softmax.  Scheduling barriers keep this order.
     u32x4 kf[2][NS];
+    if constexpr (!FP8) {
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const unsigned char* kp = sb + (2 * kk + (l32 >> 4)) * PB + (g * 16 + (l32 & 15)) * 16;
+      for (int kk = 0; kk < 2; ++kk) {
+        const unsigned char* kp = sb + (2 * kk + (l32 >> 4)) * PB + (g * 16 + (l32 & 15)) * 16;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) kf[kk][s] = ld16(kp + s * 512);
+        for (int s = 0; s < NS; ++s) kf[kk][s] = ld16(kp + s * 512);
+      }
+    } else {
+      // piece X = 4P + q (q = g or g + 2) of token t holds k-steps 4P + q/2 (bytes 0-7) and 4P + 2 + q/2
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const unsigned char* kp = sb + (2 * kk + (l32 >> 4)) * PB + (l32 & 15) * 16;
+#pragma unroll
+        for (int P = 0; P < D / 64; ++P)
+#pragma unroll
+          for (int qh = 0; qh < 2; ++qh) {
+            const u32x4 r = ld16(kp + ((4 * P + g + 2 * qh) * 16) * 16);
+            kf[kk][4 * P + qh] = cvt8(r[0], r[1]);
+            kf[kk][4 * P + 2 + qh] = cvt8(r[2], r[3]);
+          }
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     f32x16 S[2] = {f32x16{}, f32x16{}};
@@ -174,9 +226,19 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     u32x4 vf[NPG][NDT];
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) {
-      const unsigned char* vp = sb + pg * PB + 2 * KB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 512;
+      if constexpr (!FP8) {
+        const unsigned char* vp = sb + pg * PB + KBB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 512;
 #pragma unroll
-      for (int d = 0; d < NDT; ++d) vf[pg][d] = ld16(vp + d * 1024);
+        for (int d = 0; d < NDT; ++d) vf[pg][d] = ld16(vp + d * 1024);
+      } else {
+        // piece (Y = d, h = g, dim l32 % 16): bytes 8 (l32 / 16) .. +7 are this lane's 8 slots
+        const unsigned char* vp = sb + pg * PB + KBB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 8;
+#pragma unroll
+        for (int d = 0; d < NDT; ++d) {
+          const uint2 r = *reinterpret_cast<const uint2*>(vp + d * 512);
+          vf[pg][d] = cvt8(r.x, r.y);
+        }
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     // Softmax on raw scores: with c = scale * log2(e) > 0 (the host rejects other scales),
@@ -239,7 +301,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   if (bad) atomicCAS(a.err, 0, KVP_ERANGE);
   l_run += __shfl_xor(l_run, 32);
   if (!row_ok) return;
-  const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+  const float inv = l_run > 0.0f ? a.v_scale / l_run : 0.0f;
   const int64_t o = ((int64_t)(q0 + fpos) * a.Hq + it.kvh * G + hl) * D + 4 * g;
 #pragma unroll
   for (int d = 0; d < NDT; ++d)
@@ -263,8 +325,15 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 
 hipError_t launch_prefill(const PrefillArgs& a, int D, hipStream_t s) {
   if (a.n_items == 0) return hipSuccess;
-  if (D == 128) hipLaunchKernelGGL(prefill_kernel<128>, dim3(a.n_items), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(prefill_kernel<64>, dim3(a.n_items), dim3(256), 0, s, a);
+  const dim3 grid(a.n_items);
+  if (a.fp8) {
+    if (D == 128) hipLaunchKernelGGL((prefill_kernel<128, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((prefill_kernel<64, true>), grid, dim3(256), 0, s, a);
+  } else if (D == 128) {
+    hipLaunchKernelGGL((prefill_kernel<128, false>), grid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((prefill_kernel<64, false>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

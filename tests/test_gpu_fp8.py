@@ -133,3 +133,28 @@ def test_fp8_decode_bf16_out_and_determinism():
     assert torch.equal(a, b)
     ref = F.decode(c.vals.q, c.ck, c.cv, c.w.block_tables, c.w.decode_len, c.w.scale, 0.7, 1.1)
     assert_close(a, ref, "fp8 decode bf16 out")
+
+
+def _prefill(c, out_dtype=None):
+    import torch
+    w = c.w
+    s0, s1 = int(w.prefill_seqs[0]), int(w.prefill_seqs[-1]) + 1
+    out = kp.prefix_chunk_prefill_attn(to_dev_bits(c.vals.qp), c.pool, 0, c.bt[s0:s1], w.prefill_ctx, w.cu_q(),
+                                       scale=w.scale, out_dtype=out_dtype or torch.float32)
+    torch.cuda.synchronize()
+    return out
+
+
+def _oracle_prefill(c):
+    w = c.w
+    s0, s1 = int(w.prefill_seqs[0]), int(w.prefill_seqs[-1]) + 1
+    return F.prefill(c.vals.qp, c.ck, c.cv, w.block_tables[s0:s1], w.prefill_ctx, w.cu_q(), w.scale, c.ks, c.vs)
+
+
+@pytest.mark.parametrize("name,ks,vs,over", [("agentic_s", 1.0, 1.0, {}), ("mixed_s", 0.45, 1.7, {}),
+                                              ("agentic_s", 0.8, 0.9, {"d": 64})])
+def test_fp8_prefill_parity(name, ks, vs, over):
+    note(f"fp8 prefill {name} {over} scales {ks} {vs}")
+    c = Fp8Case(name, ks, vs, **over)
+    assert_close(_prefill(c), _oracle_prefill(c), f"fp8 prefill {name} {over}")
+    assert c.pool.device_error() == kp.KVP_OK
