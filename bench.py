@@ -53,13 +53,14 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle baseline sample")
     ap.add_argument("--no-flush", action="store_true", help="do not evict the Infinity Cache between steps")
+    ap.add_argument("--no-fp8", action="store_true", help="skip the FP8-KV leg (same step over an FP8 pool)")
     return ap.parse_args()
 
 
-def decode_algorithmic_bytes(w) -> int:
+def decode_algorithmic_bytes(w, kv_elem_bytes: int = 2) -> int:
     """KV bytes of every cached token decode reads, each group's shared pages counted once, plus Q, O
     (bf16) and the block-table entries referenced."""
-    kv = w.unique_decode_tokens() * w.Hkv * w.d * 2 * 2
+    kv = w.unique_decode_tokens() * w.Hkv * w.d * 2 * kv_elem_bytes
     dec = w.decode_len > 0
     qo = int(dec.sum()) * w.Hq * w.d * 2 * 2
     pages = 0
@@ -206,6 +207,58 @@ def prefix_hash_leg(kp, W, w, stream, reps: int = 5) -> dict:
             "hash_tokens_per_s": round(int(cu[-1]) / (t_hash / 1e3), 1), "lookup_ms": round(t_look, 4),
             "lookup_pages_per_s": round(pages / (t_look / 1e3), 1), "reused_tokens": int(matched.sum().item()) * 16,
             "derived_prefixes_match": ok}
+
+
+def fp8_kv_leg(kp, w, vals, gp, bt, step_batches, flush, stream, steps: int, warmup: int, bf16_decode_s: float,
+               has_prefill: bool, s0: int, s1: int, cu_q) -> dict:
+    """The same step over an FP8 (E4M3) pool of the same workload: kv_append quantises, decode and prefill
+    read one byte per KV element.  Scales stay 1 (the N(0,1) values sit well inside E4M3's range)."""
+    import torch
+    pool = kp.Pool(1, w.num_pages, w.Hkv, w.d, dtype=kp.KVP_FP8_E4M3)
+    for ab in w.setup_appends:
+        rows = torch.from_numpy(ab.src_rows).to(bt.device)
+        kp.kv_append(pool, 0, vals.kv[rows, 0].contiguous(), vals.kv[rows, 1].contiguous(), bt, ab.start_pos,
+                     ab.cu_new, group_prefix=gp if ab.use_group_prefix else None)
+    ws = torch.empty(max(1, kp.paged_decode_workspace_size(pool, w.decode_len, w.Hq, gp)), dtype=torch.uint8,
+                     device=bt.device)
+    out = torch.empty((w.B, w.Hq, w.d), dtype=torch.bfloat16, device=bt.device)
+    if has_prefill:
+        pf_ws = torch.empty(max(1, kp.prefix_chunk_prefill_workspace_size(pool, w.prefill_ctx, cu_q, w.Hq)),
+                            dtype=torch.uint8, device=bt.device)
+        pf_out = torch.empty((int(cu_q[-1]), w.Hq, w.d), dtype=torch.bfloat16, device=bt.device)
+    t_dec, t_pf = [], []
+    for it in range(warmup + steps):
+        flush.fill_(1)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        for k, v, ab in step_batches:
+            kp.kv_append(pool, 0, k, v, bt, ab.start_pos, ab.cu_new, group_prefix=gp if ab.use_group_prefix else None)
+        ev[0].record(stream)
+        kp.paged_decode_attn(vals.q, pool, 0, bt, w.decode_len, group_prefix=gp, scale=w.scale, out=out, ws=ws)
+        ev[1].record(stream)
+        if has_prefill:
+            kp.prefix_chunk_prefill_attn(vals.qp, pool, 0, bt[s0:s1], w.prefill_ctx, cu_q, scale=w.scale,
+                                         out=pf_out, ws=pf_ws)
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        if it >= warmup:
+            t_dec.append(ev[0].elapsed_time(ev[1]))
+            t_pf.append(ev[1].elapsed_time(ev[2]))
+    if pool.device_error() != kp.KVP_OK:
+        raise RuntimeError("device error in the FP8 leg")
+    pool.close()
+    dec_s = float(np.median(t_dec)) / 1e3
+    nbytes = decode_algorithmic_bytes(w, kv_elem_bytes=1)
+    n_dec = int((w.decode_len > 0).sum())
+    res = {"kv_dtype": "fp8 e4m3 (bf16 matrix-core operands, fp32 accumulation)",
+           "decode_ms": round(dec_s * 1e3, 4), "decode_gbs": round(nbytes / dec_s / 1e9, 2),
+           "decode_hbm_peak_frac": round(nbytes / dec_s / 1e9 / HBM_PEAK_GBS, 4),
+           "decode_tokens_per_s": round(n_dec / dec_s, 1), "decode_speedup_vs_bf16": round(bf16_decode_s / dec_s, 3),
+           "algorithmic_bytes_per_launch": nbytes}
+    if has_prefill:
+        pf_s = float(np.median(t_pf)) / 1e3
+        res["prefill_ms"] = round(pf_s * 1e3, 4)
+        res["prefill_tflops"] = round(w.prefill_flops() / pf_s / 1e12, 2)
+    return res
 
 
 def cpu_baseline(w, vals, budget_s: float):
@@ -388,6 +441,10 @@ def main():
                                    "algorithmic_bytes_per_launch": prefill_algorithmic_bytes(w),
                                    "library_gemm_tflops": gemm_tflops,
                                    "frac_of_library_gemm": round(flops / pf_s / 1e12 / gemm_tflops, 4)}
+    if not args.no_fp8:
+        res["fp8_kv"] = fp8_kv_leg(kp, w, vals, gp, bt, step_batches, flush, stream, min(args.steps, 10), 2, dec_s,
+                                   has_prefill, s0 if has_prefill else 0, s1 if has_prefill else 0,
+                                   cu_q if has_prefill else None)
     res["kv_tier"] = kv_tier_leg(kp, pool, w, stream)
     res["prefix_hash"] = prefix_hash_leg(kp, W, w, stream)
     if not args.no_cpu_baseline:
