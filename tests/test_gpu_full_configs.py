@@ -85,3 +85,35 @@ def test_full_prefill_sampled_rows(full):
         ref = oracle.prefill_seq(qp[cu[j]:cu[j + 1]], oracle.widen_bf16(k), oracle.widen_bf16(v), w.scale, ctx,
                                  rows=rows)
         assert_close(out[cu[j] + rows], ref, f"full prefill {w.name} session {j} ({len(rows)} rows)")
+
+
+def test_full_mixed_fp8_decode_sampled():
+    """The mixed step over an FP8 pool at full size (the benchmark's FP8 leg): sampled sequences against
+    the oracle's attention over the dequantised values (quantised by the oracle from the same bf16)."""
+    import torch
+    from oracle import fp8 as F
+    w = W.make_workload("mixed")
+    vals = W.make_values(w, values="torch", device=torch.device("cuda:0"))
+    note("full mixed fp8 decode")
+    pool = kp.Pool(1, w.num_pages, w.Hkv, w.d, dtype=kp.KVP_FP8_E4M3)
+    bt = torch.from_numpy(w.block_tables).cuda()
+    gp = kp.group_prefix(w.group_id, w.shared_pages)
+    for ab in w.setup_appends + w.step_appends:
+        rows = torch.from_numpy(ab.src_rows).cuda()
+        kp.kv_append(pool, 0, vals.kv[rows, 0].contiguous(), vals.kv[rows, 1].contiguous(), bt, ab.start_pos,
+                     ab.cu_new, group_prefix=gp if ab.use_group_prefix else None)
+    out = kp.paged_decode_attn(vals.q, pool, 0, bt, w.decode_len, group_prefix=gp, scale=w.scale,
+                               out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert pool.device_error() == kp.KVP_OK
+    out = out.float().cpu().numpy().astype(np.float64)
+    q = W.to_numpy_bits(vals.q)
+    seqs = sample_seqs(w)
+    ref = []
+    for i in seqs:
+        kb, vb = W.seq_kv_bits(w, vals, i, int(w.decode_len[i]))
+        k = F.dequantize(F.quantize_bf16(kb, 1.0), 1.0)
+        v = F.dequantize(F.quantize_bf16(vb, 1.0), 1.0)
+        ref.append(oracle.decode_seq(q[i], k, v, w.scale))
+    assert_close(out[seqs], np.stack(ref), f"full mixed fp8 decode ({len(seqs)} sampled sequences)")
+    pool.close()
