@@ -83,30 +83,34 @@ def prefill_algorithmic_bytes(w) -> int:
 
 PROFILE_OF = {"mixed": "decode_prefill_mixed_step.md", "rlvr": "decode_rlvr_64x8.md",
               "agentic": "decode_prefill_agentic_32x128k.md"}
-KERNEL_SOURCES = ("decode.hip", "prefill.hip", "plan.cpp", "kvp_layout.h", "kvp_kernels.h", "kvp_plan.h")
+KERNEL_SOURCES = ("decode.hip", "prefill.hip", "plan.cpp", "api.cpp", "kvp_layout.h", "kvp_kernels.h", "kvp_plan.h")
 
 
-def profiled_traffic(workload: str):
-    """Per-launch HBM bytes (FETCH_SIZE x2 + WRITE_SIZE, see the profile summary) for this workload, or
-    (None, None) when no summary exists or the kernel sources changed since the counters were taken."""
+def profiled_traffic(workload: str) -> dict:
+    """Per-launch HBM bytes (FETCH_SIZE x2 + WRITE_SIZE, see the profile summary) for this workload:
+    {"decode", "prefill", "decode_fp8", "prefill_fp8"} -> bytes, each None when the summary lacks it.
+    All None when no summary exists or the kernel sources changed since the counters were taken."""
     import hashlib
+    keys = {"traffic-decode-bytes": "decode", "traffic-prefill-bytes": "prefill",
+            "traffic-decode-fp8-bytes": "decode_fp8", "traffic-prefill-fp8-bytes": "prefill_fp8"}
+    res = {v: None for v in keys.values()}
     path = os.path.join(ROOT, "profiles", PROFILE_OF.get(workload, "-"))
     if not os.path.exists(path):
-        return None, None
+        return res
     fields = {}
     for line in open(path):
-        if ":" in line and line.split(":")[0].strip() in ("kernel-source-sha256", "traffic-decode-bytes",
-                                                           "traffic-prefill-bytes"):
+        if ":" in line and line.split(":")[0].strip() in (("kernel-source-sha256",) + tuple(keys)):
             k, v = line.split(":", 1)
             fields[k.strip()] = v.strip()
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
         h.update(open(os.path.join(ROOT, "paper_2608_11152_amd", "csrc", f), "rb").read())
     if fields.get("kernel-source-sha256") != h.hexdigest():
-        return None, None
-    dec = fields.get("traffic-decode-bytes")
-    pf = fields.get("traffic-prefill-bytes")
-    return (int(float(dec)) if dec else None), (int(float(pf)) if pf else None)
+        return res
+    for k, name in keys.items():
+        if fields.get(k):
+            res[name] = int(float(fields[k]))
+    return res
 
 
 def library_gemm_tflops(dev, stream, n: int = 16384, reps: int = 5) -> float:
@@ -392,7 +396,8 @@ def main():
     del src, dst
     gemm_tflops = library_gemm_tflops(dev, stream) if has_prefill else None
 
-    traffic_dec, traffic_pf = profiled_traffic(args.workload)
+    traffic = profiled_traffic(args.workload)
+    traffic_dec, traffic_pf = traffic["decode"], traffic["prefill"]
     dec_bytes = decode_algorithmic_bytes(w)
     dec_s = float(np.median(t_dec)) / 1e3
     dec_gbs = dec_bytes / dec_s / 1e9
@@ -445,6 +450,9 @@ def main():
         res["fp8_kv"] = fp8_kv_leg(kp, w, vals, gp, bt, step_batches, flush, stream, min(args.steps, 10), 2, dec_s,
                                    has_prefill, s0 if has_prefill else 0, s1 if has_prefill else 0,
                                    cu_q if has_prefill else None)
+        res["fp8_kv"]["decode_traffic"] = traffic["decode_fp8"]
+        if has_prefill:
+            res["fp8_kv"]["prefill_traffic"] = traffic["prefill_fp8"]
     res["kv_tier"] = kv_tier_leg(kp, pool, w, stream)
     res["prefix_hash"] = prefix_hash_leg(kp, W, w, stream)
     if not args.no_cpu_baseline:
