@@ -158,3 +158,80 @@ def test_fp8_prefill_parity(name, ks, vs, over):
     c = Fp8Case(name, ks, vs, **over)
     assert_close(_prefill(c), _oracle_prefill(c), f"fp8 prefill {name} {over}")
     assert c.pool.device_error() == kp.KVP_OK
+
+
+@pytest.mark.parametrize("G,members,d", [(8, 3, 128), (16, 2, 128), (4, 12, 64), (1, 80, 64), (2, 5, 128),
+                                         (8, 9, 128)])
+def test_fp8_decode_group_shapes(G, members, d):
+    """FP8 pages under every shared-prefix tiling (LDS-staged 2-3 column tiles, subgroups, G = 1 / 16,
+    odd member counts, page ranges that end inside a four-page step)."""
+    import torch
+    import oracle
+    Hkv = 2
+    Hq = G * Hkv
+    ks, vs = 0.6, 1.4
+    rng = np.random.default_rng(G * 1000 + members + d)
+    P = int(rng.integers(40, 300))
+    S = P // 16
+    priv = rng.integers(1, 500, size=members)
+    lens = (P + priv).astype(np.int32)
+    pages = [(int(n) + 15) // 16 for n in lens]
+    num_pages = S + sum(p - S for p in pages) + 7
+    perm = rng.permutation(num_pages).astype(np.int32)
+    bt = np.full((members, max(pages)), -1, np.int32)
+    nxt = S
+    for i in range(members):
+        bt[i, :S] = perm[:S]
+        k = pages[i] - S
+        bt[i, S:S + k] = perm[nxt:nxt + k]
+        nxt += k
+    prompt = W.f32_to_bf16_bits(rng.standard_normal((P, 2, Hkv, d), dtype=np.float32))
+    own = [W.f32_to_bf16_bits(rng.standard_normal((int(priv[i]), 2, Hkv, d), dtype=np.float32)) for i in range(members)]
+    qb = W.f32_to_bf16_bits(rng.standard_normal((members, Hq, d), dtype=np.float32))
+    pool = kp.Pool(1, num_pages, Hkv, d, dtype=kp.KVP_FP8_E4M3)
+    pool.set_scales(0, ks, vs)
+    btd = torch.from_numpy(bt).cuda()
+    note(f"fp8 group shapes G={G} members={members} d={d} P={P}")
+    cnt0 = np.zeros(members, np.int64)
+    cnt0[0] = S * 16
+    kv0 = to_dev_bits(prompt[:S * 16])
+    kp.kv_append(pool, 0, kv0[:, 0].contiguous(), kv0[:, 1].contiguous(), btd, np.zeros(members, np.int32),
+                 np.concatenate([[0], np.cumsum(cnt0)]).astype(np.int32))
+    rest = [np.concatenate([prompt[S * 16:], own[i]]) for i in range(members)]
+    kv1 = to_dev_bits(np.concatenate(rest))
+    cu1 = np.concatenate([[0], np.cumsum([len(r) for r in rest])]).astype(np.int32)
+    gp = kp.group_prefix(np.zeros(members, np.int32), np.array([S], np.int32))
+    kp.kv_append(pool, 0, kv1[:, 0].contiguous(), kv1[:, 1].contiguous(), btd, np.full(members, S * 16, np.int32),
+                 cu1, group_prefix=gp)
+    out = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, lens, group_prefix=gp, scale=0.11)
+    out_ng = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, lens, scale=0.11)
+    torch.cuda.synchronize()
+    assert pool.device_error() == kp.KVP_OK
+    ref = []
+    for i in range(members):
+        x = np.concatenate([prompt, own[i]])
+        k = F.dequantize(F.quantize_bf16(x[:, 0], ks), ks)
+        v = F.dequantize(F.quantize_bf16(x[:, 1], vs), vs)
+        ref.append(oracle.decode_seq(qb[i], k, v, 0.11))
+    ref = np.stack(ref)
+    assert_close(out, ref, f"fp8 group G={G} x{members} d={d}")
+    assert_close(out_ng, ref, f"fp8 ungrouped G={G} x{members} d={d}")
+
+
+def test_fp8_pool_tier_round_trip():
+    """The host tier moves FP8 pages as bytes: offload, wipe, restore gives the same pool and decode."""
+    import torch
+    c = Fp8Case("mixed_s", 0.9, 1.1)
+    note("fp8 tier round trip")
+    ref = _decode(c)
+    pb = kp.kv_pool_page_bytes(c.pool)
+    assert pb == c.w.Hkv * 32 * c.w.d
+    raw0 = c.pool.layer_bytes().clone()
+    used = sorted({int(x) for x in c.w.block_tables[c.w.block_tables >= 0]})
+    host = torch.empty(len(used) * pb, dtype=torch.uint8, pin_memory=True)
+    kp.kv_offload(c.pool, 0, used, host)
+    c.pool.reset()
+    kp.kv_restore(c.pool, 0, host, used)
+    torch.cuda.synchronize()
+    assert torch.equal(c.pool.layer_bytes(), raw0)
+    assert torch.equal(_decode(c), ref)
