@@ -308,8 +308,8 @@ def cpu_baseline(w, vals, budget_s: float):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is design-only "
-                                   "(see the sharding section of DESIGN.md)", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "the library runs on one GPU; sharding across GPUs is not implemented, so "
+                                   "--gpus must be 1", "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
 
