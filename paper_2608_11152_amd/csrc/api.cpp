@@ -235,6 +235,28 @@ int lease_seq_info(const int32_t* cu_tokens, int num_seqs, Staging::Lease* lease
   return KVP_OK;
 }
 
+// 64-page chunks of every sequence's full pages (block hashing and prefix lookup work per chunk);
+// pad = {the sequence's chunk count, the sequence, its full pages}.
+int build_chunks(const int32_t* cu_tokens, int num_seqs, std::vector<kvp::HashChunk>* chunks, int64_t* pages) {
+  if (!cu_tokens) return set_err(KVP_EINVAL, "cu_tokens is NULL");
+  if (cu_tokens[0] != 0) return set_err(KVP_EINVAL, "cu_tokens[0] = %d, must be 0", cu_tokens[0]);
+  int64_t tot = 0;
+  for (int i = 0; i < num_seqs; ++i) {
+    const int32_t n = cu_tokens[i + 1] - cu_tokens[i];
+    if (n < 0) return set_err(KVP_EINVAL, "cu_tokens decreases at %d", i);
+    const int np = n / kvp::kPage;
+    const int g0 = (int)chunks->size();
+    const int nch = (np + 63) / 64;
+    for (int c = 0; c < nch; ++c)
+      chunks->push_back(kvp::HashChunk{cu_tokens[i] + 64 * kvp::kPage * c, (int32_t)(tot + 64 * c),
+                                       std::min(64, np - 64 * c), c, g0, {nch, i, np}});
+    tot += np;
+    if (tot > INT32_MAX) return set_err(KVP_EINVAL, "more than 2^31 pages");
+  }
+  *pages = tot;
+  return KVP_OK;
+}
+
 // Page moves between the pool and the host tier: the item list is read by the kernel straight from a
 // pinned staging slot, released after the kernel.
 int run_tier(kvp_pool_t pool, int layer, const std::vector<kvp::TierItem>& items, void* host, int32_t* bt,
@@ -606,23 +628,32 @@ int kvp_block_hashes(const int32_t* tokens, const int32_t* cu_tokens, int num_se
                      uint64_t* hashes, void* stream) {
   if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
   if (num_seqs == 0) return KVP_OK;
-  Staging::Lease lease;
+  std::vector<kvp::HashChunk> chunks;
   int64_t pages = 0;
-  size_t off = 0;
-  int rc = lease_seq_info(cu_tokens, num_seqs, &lease, &pages, {}, &off);
-  if (rc) return rc;
+  int rc0 = build_chunks(cu_tokens, num_seqs, &chunks, &pages);
+  if (rc0) return rc0;
+  if (pages == 0) return KVP_OK;
+  if (!tokens || !hashes) return set_err(KVP_EINVAL, "tokens or hashes is NULL");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (pages == 0) return staging().release(lease, s, false);
-  if (!tokens || !hashes) {
+  Staging::Lease lease;
+  const size_t nb = chunks.size() * sizeof(kvp::HashChunk);
+  int rc = staging().lease(nb, &lease);
+  if (rc) return rc;
+  std::memcpy(lease.host, chunks.data(), nb);
+  void* totals = nullptr;
+  hipError_t e = hipMallocAsync(&totals, chunks.size() * 16, s);
+  if (e != hipSuccess) {
     (void)staging().release(lease, s, false);
-    return set_err(KVP_EINVAL, "tokens or hashes is NULL");
+    return set_err(KVP_ENOMEM, "hipMallocAsync(%zu): %s", chunks.size() * 16, hipGetErrorString(e));
   }
   kvp::HashArgs a{};
   a.tokens = tokens;
-  a.seq_info = reinterpret_cast<const int4*>(reinterpret_cast<unsigned char*>(lease.host) + off);
+  a.chunks = reinterpret_cast<const kvp::HashChunk*>(lease.host);
   a.seed = seed;
   a.out = hashes;
-  hipError_t e = kvp::launch_block_hash(a, num_seqs, s);
+  a.totals = reinterpret_cast<uint64_t*>(totals);
+  e = kvp::launch_block_hash(a, (int)chunks.size(), s);
+  (void)hipFreeAsync(totals, s);
   const int rr = staging().release(lease, s, e == hipSuccess);
   if (e != hipSuccess) return hip_err(e, "kvp_block_hashes launch");
   return rr;
@@ -759,26 +790,47 @@ int kvp_prefix_lookup(kvp_prefix_table_t t, const uint64_t* hashes, const int32_
   if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
   if (num_seqs == 0) return KVP_OK;
   if (!matched_pages) return set_err(KVP_EINVAL, "matched_pages is NULL");
-  Staging::Lease lease;
+  std::vector<kvp::HashChunk> chunks;
   int64_t pages = 0;
-  size_t off = 0;
-  int rc = lease_seq_info(cu_tokens, num_seqs, &lease, &pages, {}, &off);
+  int rc = build_chunks(cu_tokens, num_seqs, &chunks, &pages);
   if (rc) return rc;
+  if (pages > 0 && (!hashes || !page_ids)) return set_err(KVP_EINVAL, "hashes or page_ids is NULL");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (pages > 0 && (!hashes || !page_ids)) {
+  // Sequences without a full page match nothing: give them a zero-length chunk so pass 2 reports 0.
+  for (int i = 0, k = 0; i < num_seqs; ++i) {
+    while (k < (int)chunks.size() && chunks[k].pad[1] < i) ++k;
+    if (k == (int)chunks.size() || chunks[k].pad[1] != i) {
+      chunks.insert(chunks.begin() + k, kvp::HashChunk{0, 0, 0, 0, 0, {1, i, 0}});
+    }
+  }
+  for (size_t k = 0; k < chunks.size(); ++k)  // g0 must index this sequence's first chunk after inserts
+    if (chunks[k].c == 0) {
+      const int g0 = (int)k;
+      for (size_t j = k; j < chunks.size() && chunks[j].pad[1] == chunks[k].pad[1]; ++j) chunks[j].g0 = g0;
+    }
+  Staging::Lease lease;
+  const size_t nb = chunks.size() * sizeof(kvp::HashChunk);
+  rc = staging().lease(nb, &lease);
+  if (rc) return rc;
+  std::memcpy(lease.host, chunks.data(), nb);
+  void* scratch = nullptr;
+  hipError_t e = hipMallocAsync(&scratch, chunks.size() * 4, s);
+  if (e != hipSuccess) {
     (void)staging().release(lease, s, false);
-    return set_err(KVP_EINVAL, "hashes or page_ids is NULL");
+    return set_err(KVP_ENOMEM, "hipMallocAsync(%zu): %s", chunks.size() * 4, hipGetErrorString(e));
   }
   kvp::TableArgs a{};
   a.keys = t->keys;
   a.vals = t->vals;
   a.mask = t->mask;
   a.hashes = hashes;
-  a.seq_info = reinterpret_cast<const int4*>(reinterpret_cast<unsigned char*>(lease.host) + off);
+  a.chunks = reinterpret_cast<const kvp::HashChunk*>(lease.host);
+  a.first_miss = reinterpret_cast<int32_t*>(scratch);
   a.matched = matched_pages;
   a.out_pages = page_ids;
   a.err = t->err;
-  hipError_t e = kvp::launch_table(a, 2, num_seqs, s);
+  e = kvp::launch_table(a, 2, (int)chunks.size(), s);
+  (void)hipFreeAsync(scratch, s);
   const int rr = staging().release(lease, s, e == hipSuccess);
   if (e != hipSuccess) return hip_err(e, "kvp_prefix_lookup launch");
   return rr;

@@ -113,12 +113,22 @@ struct TierArgs {
   int maxp;
 };
 
-// Block hashing: per sequence {first token, full pages, first output slot, 0}.
+// Block hashing works on chunks of up to 64 full pages of one sequence.
+struct HashChunk {
+  int32_t t0;               // first token of the chunk
+  int32_t o0;               // first output slot of the chunk
+  int32_t n;                // pages in the chunk (1..64)
+  int32_t c;                // chunk index within its sequence
+  int32_t g0;               // index of the sequence's first chunk in `totals`
+  int32_t pad[3];           // lookup: the sequence's chunk count, the sequence, its full pages
+};
+
 struct HashArgs {
   const int32_t* tokens;
-  const int4* seq_info;     // [num_seqs] (pinned host)
+  const HashChunk* chunks;  // [n_chunks] (pinned host)
   uint64_t seed;
-  uint64_t* out;            // [total full pages]
+  uint64_t* out;            // [total full pages]; chunk-local chain values between the two passes
+  uint64_t* totals;         // [2 * n_chunks] scratch: each chunk's composed map (slope, offset)
 };
 
 struct GroupLcpArgs {
@@ -136,7 +146,8 @@ struct TableArgs {
   const uint64_t* hashes;   // insert / erase: [n]; lookup: per-page hashes laid out as seq_info says
   const int32_t* pages;     // insert / erase: [n]
   int64_t n;
-  const int4* seq_info;     // lookup
+  const HashChunk* chunks;  // lookup: 64-page chunks of the sequences (pinned host)
+  int32_t* first_miss;      // lookup scratch: [chunks]
   int32_t* matched;         // lookup: [num_seqs]
   int32_t* out_pages;       // lookup: [total full pages]
   int* err;
@@ -149,7 +160,7 @@ hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s);
 hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s);
 hipError_t launch_prefill(const PrefillArgs& a, int D, hipStream_t s);
 hipError_t launch_tier(const TierArgs& a, bool restore, hipStream_t s);
-hipError_t launch_block_hash(const HashArgs& a, int n_seqs, hipStream_t s);
+hipError_t launch_block_hash(const HashArgs& a, int n_chunks, hipStream_t s);
 hipError_t launch_group_lcp(const GroupLcpArgs& a, int n_groups, hipStream_t s);
 // op: 0 insert, 1 erase, 2 lookup, 3 clear
 hipError_t launch_table(const TableArgs& a, int op, int n_seqs, hipStream_t s);
