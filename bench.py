@@ -355,15 +355,21 @@ def main():
             kp.kv_append(pool, 0, k, v, bt, ab.start_pos, ab.cu_new, group_prefix=gp if ab.use_group_prefix else None)
         if ev:
             ev[1].record(stream)
+        h0 = time.perf_counter()
         kp.paged_decode_attn(vals.q, pool, 0, bt, w.decode_len, group_prefix=gp, scale=w.scale, out=dec_out,
                              ws=dec_ws)
+        h1 = time.perf_counter()
         if ev:
             ev[2].record(stream)
         if has_prefill:
             kp.prefix_chunk_prefill_attn(vals.qp, pool, 0, bt[s0:s1], w.prefill_ctx, cu_q, scale=w.scale,
                                          out=pf_out, ws=pf_ws)
+        h2 = time.perf_counter()
         if ev:
             ev[3].record(stream)
+            host_ms.append(((h1 - h0) * 1e3, (h2 - h1) * 1e3))
+
+    host_ms = []  # host time of each call: validation, planning, packing and launch (it returns before the GPU)
 
     for _ in range(args.warmup):
         step()
@@ -425,6 +431,8 @@ def main():
                       "p10": round(float(np.percentile(t_dec, 10)), 4),
                       "p90": round(float(np.percentile(t_dec, 90)), 4)},
         "append_ms": round(float(np.median(t_app)), 4),
+        "host_call_ms": {"paged_decode_attn": round(float(np.median([h[0] for h in host_ms])), 4),
+                         "prefix_chunk_prefill_attn": round(float(np.median([h[1] for h in host_ms])), 4)},
         "hbm_copy_gbs": round(copy_gbs, 1),
         "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic_dec,
