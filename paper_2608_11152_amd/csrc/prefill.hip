@@ -106,23 +106,27 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   // scalar loads, index clamped into the tile's page range so each is in bounds.  A missing or invalid
   // page is read from page 0 and `patch` zeroes it once the copies have landed, together with the slots
   // past the end of the sequence in its last page (stale pool contents).
-  auto fetch = [&](int st, int buf, bool (&okp)[NPG]) {
+  auto fetch = [&](int st, int buf, unsigned& okm) {
+    okm = 0u;
     int ids[NPG];
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) ids[pg] = btr[min(st * NPG + pg, n_pages - 1)];
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) {
       const bool inr = st * NPG + pg < n_pages;
-      okp[pg] = inr && (unsigned)ids[pg] < (unsigned)a.num_pages;
-      bad |= inr && !okp[pg];
-      ids[pg] = okp[pg] ? ids[pg] : 0;
+      const bool ok = inr && (unsigned)ids[pg] < (unsigned)a.num_pages;
+      okm |= ok ? 1u << pg : 0u;
+      bad |= inr && !ok;
+      ids[pg] = ok ? ids[pg] : 0;
       if constexpr (CPP >= 1) {
-        const unsigned char* src = hbase + (int64_t)ids[pg] * page_stride + tid * 16;
+        // wave-uniform page base + a 32-bit lane offset, and a wave-uniform LDS base: the address
+        // arithmetic stays scalar
+        const unsigned char* pbase = hbase + (int64_t)ids[pg] * page_stride;
 #pragma unroll
         for (int c = 0; c < CPP; ++c) {
           const int k = pg * CPP + c;
-          __builtin_amdgcn_global_load_lds(src + c * (256 * 16),
-                                           (__attribute__((address_space(3))) void*)(lds + buf * SB + k * 4096 + wv * 1024),
+          __builtin_amdgcn_global_load_lds(pbase + (uint32_t)(c * 4096 + tid * 16),
+                                           (__attribute__((address_space(3))) void*)(lds + buf * SB + k * 4096 + wvu * 1024),
                                            16, 0, 0);
         }
       }
@@ -137,17 +141,14 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       }
     }
   };
-  auto patch = [&](int st, int buf, const bool (&okp)[NPG]) {
-    bool any = (st + 1) * NPG * 16 > seq_tokens;
-#pragma unroll
-    for (int pg = 0; pg < NPG; ++pg) any |= !okp[pg];
-    if (!any) return;
+  auto patch = [&](int st, int buf, unsigned okm) {
+    if ((st + 1) * NPG * 16 <= seq_tokens && okm == (1u << NPG) - 1u) return;
     // Piece k of this thread: stage bytes [4096k + 16 tid, +16), in page (4096k + 1024 wv) / PB.
 #pragma unroll
     for (int k = 0; k < NCH; ++k) {
       const int o = k * 4096 + wvu * 1024;
       const int pg = o / PB;
-      const int valid = okp[pg] ? seq_tokens - (st * NPG + pg) * 16 : 0;  // usable tokens of this page
+      const int valid = (okm >> pg) & 1u ? seq_tokens - (st * NPG + pg) * 16 : 0;  // usable tokens of this page
       if (valid >= 16) continue;
       {
         const int inb = (o % PB) + lane * 16;
@@ -180,15 +181,15 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   // vmcnt(0): the stage's LDS copies have landed (expcnt / lgkmcnt left unconstrained).
   auto wait_copies = [] { __builtin_amdgcn_s_waitcnt(0x0F70); };
 
-  bool okp[NPG];
-  fetch(0, 0, okp);
+  unsigned okm;  // bit pg: page pg of the stage in flight is valid
+  fetch(0, 0, okm);
   wait_copies();
-  patch(0, 0, okp);
+  patch(0, 0, okm);
   __syncthreads();
   int buf = 0;
   for (int st = 0; st < n_stages; ++st) {
     const bool more = st + 1 < n_stages;
-    if (more) fetch(st + 1, buf ^ 1, okp);
+    if (more) fetch(st + 1, buf ^ 1, okm);
     const unsigned char* sb = lds + buf * SB;
     // K operand fragments for both 32-key tiles are read from LDS up front, then the two independent
     // MFMA chains are interleaved; the V fragments are read next so their latency hides behind the
@@ -241,8 +242,12 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       }
     }
     __builtin_amdgcn_sched_barrier(0);
-    // Softmax on raw scores: with c = scale * log2(e) > 0 (the host rejects other scales),
-    // max(c*s) = c*max(s), so one FMA per score feeds exp2.
+    // Softmax against a reference max.  With c = scale * log2(e) > 0 (the host rejects other scales),
+    // the weights are exp2(c*s - m_run), m_run being the running row max of the earlier stages (exact
+    // from stage 0 on, since every row sees key 0 there).  The stage's own max is taken only at stage 0
+    // or when a lane's weight sum passes 256 (some score rose above m_run): otherwise every weight is at
+    // most 256 and, numerator and denominator sharing the reference, the result is unchanged.  So the
+    // common path has no max reduction: one FMA and one exponential per score.
     float t[32];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
@@ -258,34 +263,42 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
           if (key > qpos) t[kk * 16 + i] = -INFINITY;
         }
     }
-    float mx = fmaxf(fmaxf(t[0], t[1]), t[2]);
+    u32x4 pb[NPG];
+    float ssum = 0.0f;
+    auto weights = [&](float mr) {
+      ssum = 0.0f;
 #pragma unroll
-    for (int i = 3; i < 31; i += 2) mx = fmaxf(fmaxf(mx, t[i]), t[i + 1]);
-    mx = fmaxf(mx, t[31]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * cs;
-    const bool need = mx > m_run + 8.0f;
-    if (__any(need)) {
-      const float alpha = need ? fast_exp2(m_run - mx) : 1.0f;
-      m_run = need ? mx : m_run;
+      for (int pg = 0; pg < NPG; ++pg) {
+        float p[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          p[j] = fast_exp2(__builtin_fmaf(t[(pg >> 1) * 16 + (pg & 1) * 8 + j], cs, -mr));
+          ssum += p[j];
+        }
+#pragma unroll
+        for (int w = 0; w < 4; ++w) pb[pg][w] = pack_bf16(p[2 * w], p[2 * w + 1]);
+      }
+    };
+    bool slow = st == 0;
+    if (!slow) {
+      weights(m_run);
+      slow = __any(!(ssum <= 256.0f));
+    }
+    if (slow) {
+      float mx = fmaxf(fmaxf(t[0], t[1]), t[2]);
+#pragma unroll
+      for (int i = 3; i < 31; i += 2) mx = fmaxf(fmaxf(mx, t[i]), t[i + 1]);
+      mx = fmaxf(mx, t[31]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * cs;
+      const float mnew = fmaxf(m_run, mx);
+      const float alpha = fast_exp2(m_run - mnew);  // 0 at stage 0 (m_run = -inf), where acc and l are 0
+      m_run = mnew;
       l_run *= alpha;
 #pragma unroll
       for (int d = 0; d < NDT; ++d) acc[d] *= alpha;
+      weights(m_run);
     }
-    const float mr = (m_run == -INFINITY) ? 0.0f : m_run;
-    u32x4 pb[NPG];
-#pragma unroll
-    for (int pg = 0; pg < NPG; ++pg) {
-      float p[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        p[j] = fast_exp2(__builtin_fmaf(t[(pg >> 1) * 16 + (pg & 1) * 8 + j], cs, -mr));
-        l_run += p[j];
-      }
-      pb[pg][0] = pack_bf16(p[0], p[1]);
-      pb[pg][1] = pack_bf16(p[2], p[3]);
-      pb[pg][2] = pack_bf16(p[4], p[5]);
-      pb[pg][3] = pack_bf16(p[6], p[7]);
-    }
+    l_run += ssum;
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) {
 #pragma unroll
@@ -293,7 +306,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     }
     if (more) {
       wait_copies();
-      patch(st + 1, buf ^ 1, okp);
+      patch(st + 1, buf ^ 1, okm);
     }
     __syncthreads();
     buf ^= 1;
