@@ -630,101 +630,99 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------------------
-// Log-sum-exp merge: out = sum_j acc_j 2^(m_j - m) / sum_j l_j 2^(m_j - m), m = max_j m_j, in partial
-// order (fixed, so results are deterministic).  Empty partials (m = -inf, l = 0) carry zero weight; a
-// sequence with no partial gets a zero output.  One workgroup per (sequence, KV head), started from one
-// 16-byte record {seq, first partial, partial count}.  Phase 1: 16 threads per head hold up to four
-// partials' (m, l) each in registers, reduce the max and the weight sum, and leave each partial's weight
-// 2^(m_j - m) in LDS.  Phase 2: every thread accumulates four consecutive output dims over the partials
-// with up to 16 16-byte loads in flight.
+// Log-sum-exp merge: out = sum_j acc_j 2^(m_j - m) / sum_j l_j 2^(m_j - m), m = max_j m_j, in a fixed
+// order (so results are deterministic).  Empty partials (m = -inf, l = 0) carry zero weight; a
+// sequence with no partial gets a zero output.  One workgroup per (sequence, KV head, pair of query
+// heads), started from one 16-byte record {seq, first partial, partial count}, so that every load of a
+// workgroup is issued in one or two rounds.  Phase 1: one wave per head reduces the partials' max and
+// weight sum and leaves each partial's weight 2^(m_j - m) in LDS.  Phase 2: T threads share each output
+// float4, thread q taking partials q, q + T, ... with all of its loads in flight, and the T sums are
+// added across lanes.
 // ---------------------------------------------------------------------------------------------------
+constexpr int kMergeHeads = 2;  // query heads per merge workgroup (1 when G = 1)
+
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
-  constexpr int MAXW = 64;  // partial weights per head kept in LDS; more partials recompute theirs
-  __shared__ float s_w[16][MAXW];
-  __shared__ float s_m[16], s_inv[16];
-  const int grp = blockIdx.x / a.Hkv;
-  const int kvh = blockIdx.x - grp * a.Hkv;
+  constexpr int HW = kMergeHeads;
+  constexpr int MAXW = 256;  // partial weights per head kept in LDS; more partials recompute theirs
+  constexpr int V4 = D / 4;  // float4 per head row
+  __shared__ float s_w[HW][MAXW];
+  __shared__ float s_m[HW], s_inv[HW];
+  const int G = a.Hq / a.Hkv;
+  const int hw = G < HW ? G : HW;
+  const int nsplit = G / hw;
+  const int b = blockIdx.x;
+  const int rest = b / nsplit;
+  const int sub = b - rest * nsplit;
+  const int grp = rest / a.Hkv;
+  const int kvh = rest - grp * a.Hkv;
   const int4 info = reinterpret_cast<const int4*>(a.merge_info)[grp];
   const int seq = info.x, P = info.z;
   const int64_t base = info.y;
-  const int G = a.Hq / a.Hkv;
-  const int tid = threadIdx.x;
-  {
-    const int hh = tid >> 4, r = tid & 15;
-    const int h = kvh * G + hh;
-    const bool on = hh < G;
-    float2 ml[4];
+  const int h0 = kvh * G + sub * hw;
+  const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
+  if (wv < hw) {
+    const int h = h0 + wv;
     float m = -INFINITY;
+    for (int j = lane; j < P; j += 64) m = fmaxf(m, a.part_ml[(base + j) * a.Hq + h].x);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int j = r + 16 * k;
-      ml[k] = (on && j < P) ? a.part_ml[(base + j) * a.Hq + h] : make_float2(-INFINITY, 0.0f);
-      m = fmaxf(m, ml[k].x);
-    }
-    if (on)
-      for (int j = r + 64; j < P; j += 16) m = fmaxf(m, a.part_ml[(base + j) * a.Hq + h].x);
-#pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 16));
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
     float l = 0.0f;
-    if (on && m != -INFINITY) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int j = r + 16 * k;
-        if (j < P) {
-          const float w = fast_exp2(ml[k].x - m);
-          l += w * ml[k].y;
-          s_w[hh][j] = w;
-        }
-      }
-      for (int j = r + 64; j < P; j += 16) {
+    if (m != -INFINITY) {
+      for (int j = lane; j < P; j += 64) {
         const float2 x = a.part_ml[(base + j) * a.Hq + h];
-        l += fast_exp2(x.x - m) * x.y;
+        const float w = fast_exp2(x.x - m);
+        l += w * x.y;
+        if (j < MAXW) s_w[wv][j] = w;
       }
     }
 #pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) l += __shfl_xor(l, o, 16);
-    if (on && r == 0) {
-      s_m[hh] = m;
-      s_inv[hh] = (m != -INFINITY && l > 0.0f) ? 1.0f / l : 0.0f;
+    for (int o = 32; o >= 1; o >>= 1) l += __shfl_xor(l, o);
+    if (lane == 0) {
+      s_m[wv] = m;
+      s_inv[wv] = (m != -INFINITY && l > 0.0f) ? 1.0f / l : 0.0f;
     }
   }
   __syncthreads();
-  constexpr int V4 = D / 4;  // float4 per head row
-  constexpr int U = 16;      // partial loads in flight per thread
-  for (int e = tid; e < G * V4; e += 256) {
-    const int hh = e / V4, d4 = e - hh * V4;
-    const int h = kvh * G + hh;
-    const float m = s_m[hh], inv = s_inv[hh];
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    if (inv > 0.0f) {
-      const float* pa = a.part_acc + (base * a.Hq + h) * D + 4 * d4;
-      const int64_t sa = (int64_t)a.Hq * D;
-      for (int j0 = 0; j0 < P; j0 += U) {
-        f32x4 v[U];
+  constexpr int U = 16;                  // partial loads in flight per thread
+  const int T = 256 / (hw * V4);         // threads per output float4: 4, 8 or 16
+  const int e = tid / T, q = tid - e * T;
+  const int hh = e / V4, d4 = e - hh * V4;
+  const int h = h0 + hh;
+  const float m = s_m[hh], inv = s_inv[hh];
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (inv > 0.0f) {
+    const int64_t sa = (int64_t)a.Hq * D;
+    const float* pa = a.part_acc + (base * a.Hq + h) * D + 4 * d4;
+    for (int j0 = q; j0 < P; j0 += U * T) {
+      f32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-          if (j0 + u < P) v[u] = *reinterpret_cast<const f32x4*>(pa + (j0 + u) * sa);
+      for (int u = 0; u < U; ++u)
+        if (j0 + u * T < P) v[u] = *reinterpret_cast<const f32x4*>(pa + (j0 + u * T) * sa);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int j = j0 + u;
-          if (j < P) {
-            const float w = j < MAXW ? s_w[hh][j] : fast_exp2(a.part_ml[(base + j) * a.Hq + h].x - m);
-            acc += w * v[u];
-          }
+      for (int u = 0; u < U; ++u) {
+        const int j = j0 + u * T;
+        if (j < P) {
+          const float w = j < MAXW ? s_w[hh][j] : fast_exp2(a.part_ml[(base + j) * a.Hq + h].x - m);
+          acc += w * v[u];
         }
       }
     }
-    acc *= inv;
-    const int64_t oi = ((int64_t)seq * a.Hq + h) * D + 4 * d4;
-    if (a.out_f32) {
-      *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + oi) = acc;
-    } else {
-      uint2 u;
-      u.x = pack_bf16(acc[0], acc[1]);
-      u.y = pack_bf16(acc[2], acc[3]);
-      *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + oi) = u;
-    }
+  }
+  // the T partial sums of an output sit in T consecutive lanes
+  for (int o = T >> 1; o >= 1; o >>= 1)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] += __shfl_xor(acc[c], o);
+  if (q != 0) return;
+  acc *= inv;
+  const int64_t oi = ((int64_t)seq * a.Hq + h) * D + 4 * d4;
+  if (a.out_f32) {
+    *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + oi) = acc;
+  } else {
+    uint2 u;
+    u.x = pack_bf16(acc[0], acc[1]);
+    u.y = pack_bf16(acc[2], acc[3]);
+    *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + oi) = u;
   }
 }
 
@@ -747,7 +745,9 @@ hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s) {
 
 hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s) {
   if (a.n_merge == 0) return hipSuccess;
-  const dim3 grid((unsigned)((int64_t)a.n_merge * a.Hkv));
+  const int G = a.Hq / a.Hkv;
+  const int nsplit = G / (G < kMergeHeads ? G : kMergeHeads);
+  const dim3 grid((unsigned)((int64_t)a.n_merge * a.Hkv * nsplit));
   if (D == 128) hipLaunchKernelGGL(decode_merge_kernel<128>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(256), 0, s, a);
   return hipGetLastError();

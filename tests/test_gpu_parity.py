@@ -228,6 +228,46 @@ def test_prefill_shapes(ctx, C, G):
 # edge cases and errors
 # ------------------------------------------------------------------------------------------------
 
+@pytest.mark.parametrize("pattern", ["rising", "falling", "wide"])
+def test_softmax_dynamic_range(pattern):
+    """Scores far from N(0, 1): rising along the sequence (the running max moves by more than 8 (log2) in
+    almost every 64-key stage, so the kernels rescale every stage), falling (the max is at key 0 and later
+    weights fall to 2^-100), and wide (scores of std ~50 in log2 units, weights nearly one-hot)."""
+    import torch
+    G, Hkv, d, ctx, C = 8, 2, 128, 700, 70
+    Hq, n = G * Hkv, ctx + C
+    rng = np.random.default_rng({"rising": 1, "falling": 2, "wide": 3}[pattern])
+    u = rng.standard_normal(d).astype(np.float32)
+    if pattern == "wide":
+        k = 6.0 * rng.standard_normal((n, Hkv, d)).astype(np.float32)
+        q = 6.0 * rng.standard_normal((C, Hq, d)).astype(np.float32)
+    else:
+        a = np.linspace(-6.0, 6.0, n, dtype=np.float32)
+        if pattern == "falling":
+            a = a[::-1].copy()
+        k = a[:, None, None] * u[None, None, :] + 0.3 * rng.standard_normal((n, Hkv, d)).astype(np.float32)
+        q = u[None, None, :] + 0.3 * rng.standard_normal((C, Hq, d)).astype(np.float32)
+    v = rng.standard_normal((n, Hkv, d)).astype(np.float32)
+    kvb = W.f32_to_bf16_bits(np.stack([k, v], axis=1))
+    qb = W.f32_to_bf16_bits(q)
+    npg = (n + 15) // 16
+    num_pages = npg + 3
+    bt = rng.permutation(num_pages)[:npg].astype(np.int32)[None, :]
+    pool = kp.Pool(1, num_pages, Hkv, d)
+    btd = torch.from_numpy(bt).cuda()
+    kvd = to_dev_bits(kvb)
+    note(f"softmax dynamic range {pattern}")
+    kp.kv_append(pool, 0, kvd[:, 0].contiguous(), kvd[:, 1].contiguous(), btd, [0], [0, n])
+    out = kp.prefix_chunk_prefill_attn(to_dev_bits(qb), pool, 0, btd, [ctx], [0, C], scale=0.09)
+    dec = kp.paged_decode_attn(to_dev_bits(qb[C - 1:]), pool, 0, btd, [n], scale=0.09)
+    torch.cuda.synchronize()
+    kf, vf = oracle.widen_bf16(kvb[:, 0]), oracle.widen_bf16(kvb[:, 1])
+    ref = oracle.prefill_seq(qb, kf, vf, 0.09, ctx)
+    assert np.all(np.isfinite(ref))
+    assert_close(out, ref, f"prefill {pattern}")
+    assert_close(dec, ref[C - 1:], f"decode {pattern}")
+
+
 @pytest.mark.parametrize("G,d", [(1, 128), (2, 64), (4, 128), (16, 64), (16, 128)])
 def test_decode_edge_lengths(G, d):
     """Empty, single-token, page-aligned and ragged sequences, long sequences split many ways."""
