@@ -633,23 +633,19 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 // Log-sum-exp merge: out = sum_j acc_j 2^(m_j - m) / sum_j l_j 2^(m_j - m), m = max_j m_j, in a fixed
 // order (so results are deterministic).  Empty partials (m = -inf, l = 0) carry zero weight; a
 // sequence with no partial gets a zero output.  One workgroup per (sequence, KV head, pair of query
-// heads), started from one 16-byte record {seq, first partial, partial count}, so that every load of a
-// workgroup is issued in one or two rounds.  Phase 1: one wave per head reduces the partials' max and
-// weight sum and leaves each partial's weight 2^(m_j - m) in LDS.  Phase 2: T threads share each output
-// float4, thread q taking partials q, q + T, ... with all of its loads in flight, and the T sums are
-// added across lanes.
+// heads), started from one 16-byte record {seq, first partial, partial count}.  T consecutive lanes
+// share each output float4: lane q loads partials q, q + T, ... (accumulator and (m, l) together, all
+// in flight at once), folds them with a running max, and the T lanes are then combined by shuffles, so
+// the whole merge costs one round of memory latency.
 // ---------------------------------------------------------------------------------------------------
 constexpr int kMergeHeads = 2;  // query heads per merge workgroup (1 when G = 1)
 
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
-  constexpr int HW = kMergeHeads;
-  constexpr int MAXW = 256;  // partial weights per head kept in LDS; more partials recompute theirs
   constexpr int V4 = D / 4;  // float4 per head row
-  __shared__ float s_w[HW][MAXW];
-  __shared__ float s_m[HW], s_inv[HW];
+  constexpr int U = 16;      // partials in flight per lane
   const int G = a.Hq / a.Hkv;
-  const int hw = G < HW ? G : HW;
+  const int hw = G < kMergeHeads ? G : kMergeHeads;
   const int nsplit = G / hw;
   const int b = blockIdx.x;
   const int rest = b / nsplit;
@@ -659,62 +655,58 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
   const int4 info = reinterpret_cast<const int4*>(a.merge_info)[grp];
   const int seq = info.x, P = info.z;
   const int64_t base = info.y;
-  const int h0 = kvh * G + sub * hw;
-  const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
-  if (wv < hw) {
-    const int h = h0 + wv;
-    float m = -INFINITY;
-    for (int j = lane; j < P; j += 64) m = fmaxf(m, a.part_ml[(base + j) * a.Hq + h].x);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-    float l = 0.0f;
-    if (m != -INFINITY) {
-      for (int j = lane; j < P; j += 64) {
-        const float2 x = a.part_ml[(base + j) * a.Hq + h];
-        const float w = fast_exp2(x.x - m);
-        l += w * x.y;
-        if (j < MAXW) s_w[wv][j] = w;
-      }
-    }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) l += __shfl_xor(l, o);
-    if (lane == 0) {
-      s_m[wv] = m;
-      s_inv[wv] = (m != -INFINITY && l > 0.0f) ? 1.0f / l : 0.0f;
-    }
-  }
-  __syncthreads();
-  constexpr int U = 16;                  // partial loads in flight per thread
-  const int T = 256 / (hw * V4);         // threads per output float4: 4, 8 or 16
+  const int tid = threadIdx.x;
+  const int T = 256 / (hw * V4);  // lanes per output float4: 4, 8 or 16 (a divisor of 64)
   const int e = tid / T, q = tid - e * T;
   const int hh = e / V4, d4 = e - hh * V4;
-  const int h = h0 + hh;
-  const float m = s_m[hh], inv = s_inv[hh];
+  const int h = kvh * G + sub * hw + hh;
+  const int64_t sa = (int64_t)a.Hq * D;
+  const float* pa = a.part_acc + (base * a.Hq + h) * D + 4 * d4;
+  const float2* pm = a.part_ml + base * a.Hq + h;
+  float m = -INFINITY, l = 0.0f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (inv > 0.0f) {
-    const int64_t sa = (int64_t)a.Hq * D;
-    const float* pa = a.part_acc + (base * a.Hq + h) * D + 4 * d4;
-    for (int j0 = q; j0 < P; j0 += U * T) {
-      f32x4 v[U];
+  for (int j0 = q; j0 < P; j0 += U * T) {
+    f32x4 v[U];
+    float2 ml[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (j0 + u * T < P) v[u] = *reinterpret_cast<const f32x4*>(pa + (j0 + u * T) * sa);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int j = j0 + u * T;
-        if (j < P) {
-          const float w = j < MAXW ? s_w[hh][j] : fast_exp2(a.part_ml[(base + j) * a.Hq + h].x - m);
-          acc += w * v[u];
-        }
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * T;
+      if (j < P) {
+        v[u] = *reinterpret_cast<const f32x4*>(pa + j * sa);
+        ml[u] = pm[(int64_t)j * a.Hq];
       }
     }
+    float mr = m;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (j0 + u * T < P) mr = fmaxf(mr, ml[u].x);
+    if (mr != -INFINITY) {
+      const float r = fast_exp2(m - mr);  // 0 while nothing has been seen (m = -inf)
+      acc *= r;
+      l *= r;
+      m = mr;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (j0 + u * T < P) {
+          const float w = fast_exp2(ml[u].x - m);
+          acc += w * v[u];
+          l += w * ml[u].y;
+        }
+    }
   }
-  // the T partial sums of an output sit in T consecutive lanes
-  for (int o = T >> 1; o >= 1; o >>= 1)
+  // combine the T lanes of this output (consecutive lanes of one wave)
+  float mt = m;
+  for (int o = T >> 1; o >= 1; o >>= 1) mt = fmaxf(mt, __shfl_xor(mt, o));
+  const float r = mt == -INFINITY ? 0.0f : fast_exp2(m - mt);
+  acc *= r;
+  l *= r;
+  for (int o = T >> 1; o >= 1; o >>= 1) {
+    l += __shfl_xor(l, o);
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[c] += __shfl_xor(acc[c], o);
+  }
   if (q != 0) return;
-  acc *= inv;
+  acc *= (mt != -INFINITY && l > 0.0f) ? 1.0f / l : 0.0f;
   const int64_t oi = ((int64_t)seq * a.Hq + h) * D + 4 * d4;
   if (a.out_f32) {
     *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + oi) = acc;
