@@ -632,20 +632,20 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 // ---------------------------------------------------------------------------------------------------
 // Log-sum-exp merge: out = sum_j acc_j 2^(m_j - m) / sum_j l_j 2^(m_j - m), m = max_j m_j, in a fixed
 // order (so results are deterministic).  Empty partials (m = -inf, l = 0) carry zero weight; a
-// sequence with no partial gets a zero output.  One workgroup per (sequence, KV head, pair of query
-// heads), started from one 16-byte record {seq, first partial, partial count}.  T consecutive lanes
+// sequence with no partial gets a zero output.  One workgroup per (sequence, KV head, group of hw query
+// heads), started from one 16-byte record {seq, first partial, partial count}; hw is chosen per call so
+// that few sequences still spread over enough workgroups and many do not pay for extra ones.  T = 256 /
+// (hw * D / 4) consecutive lanes
 // share each output float4: lane q loads partials q, q + T, ... (accumulator and (m, l) together, all
 // in flight at once), folds them with a running max, and the T lanes are then combined by shuffles, so
 // the whole merge costs one round of memory latency.
 // ---------------------------------------------------------------------------------------------------
-constexpr int kMergeHeads = 2;  // query heads per merge workgroup (1 when G = 1)
-
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
   constexpr int V4 = D / 4;  // float4 per head row
   constexpr int U = 16;      // partials in flight per lane
   const int G = a.Hq / a.Hkv;
-  const int hw = G < kMergeHeads ? G : kMergeHeads;
+  const int hw = a.hw;
   const int nsplit = G / hw;
   const int b = blockIdx.x;
   const int rest = b / nsplit;
@@ -656,7 +656,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
   const int seq = info.x, P = info.z;
   const int64_t base = info.y;
   const int tid = threadIdx.x;
-  const int T = 256 / (hw * V4);  // lanes per output float4: 4, 8 or 16 (a divisor of 64)
+  const int T = 256 / (hw * V4);  // lanes per output float4: 1 to 16 (a divisor of 64)
   const int e = tid / T, q = tid - e * T;
   const int hh = e / V4, d4 = e - hh * V4;
   const int h = kvh * G + sub * hw + hh;
@@ -737,11 +737,17 @@ hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s) {
 
 hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s) {
   if (a.n_merge == 0) return hipSuccess;
+  // Split the query heads of a (sequence, KV head) over up to G workgroups while the grid stays at or
+  // under 1024 workgroups; at most 256 threads' worth of float4 outputs per workgroup.
   const int G = a.Hq / a.Hkv;
-  const int nsplit = G / (G < kMergeHeads ? G : kMergeHeads);
-  const dim3 grid((unsigned)((int64_t)a.n_merge * a.Hkv * nsplit));
-  if (D == 128) hipLaunchKernelGGL(decode_merge_kernel<128>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(256), 0, s, a);
+  const int64_t units = (int64_t)a.n_merge * a.Hkv;
+  int nsplit = 1;
+  while (2 * nsplit <= G && (units * 2 * nsplit <= 1024 || G / nsplit > 1024 / D)) nsplit *= 2;
+  MergeArgs m = a;
+  m.hw = G / nsplit;
+  const dim3 grid((unsigned)(units * nsplit));
+  if (D == 128) hipLaunchKernelGGL(decode_merge_kernel<128>, grid, dim3(256), 0, s, m);
+  else hipLaunchKernelGGL(decode_merge_kernel<64>, grid, dim3(256), 0, s, m);
   return hipGetLastError();
 }
 

@@ -77,6 +77,7 @@ struct MergeArgs {
   void* out;
   int out_f32;
   int Hq, Hkv;
+  int hw;                     // query heads per merge workgroup (set by launch_decode_merge)
 };
 
 struct PrefillArgs {
