@@ -3,8 +3,9 @@
 //
 // One 4-wave workgroup per (session, KV head, 128 flattened query rows).  Query rows are flattened as
 // position * G + head-in-group, so every K/V tile loaded serves all G query heads of its KV head.  Keys
-// stream through LDS in stages of 4 pages (64 keys), double-buffered with direct global->LDS copies so
-// the next stage's reads overlap this stage's MFMA work.  Wave w owns 32 query rows:
+// stream through LDS in stages of 4 pages (64 keys), double-buffered: the next stage is loaded into
+// registers while this stage's MFMA work runs, then stored to the other buffer.  Wave w owns 32 query
+// rows:
 //   S^T (64 keys x 32 rows) = K Q^T      v_mfma_f32_32x32x16_bf16, 2 key tiles x D/16 k-steps
 //   O^T (D x 32 rows)      += V^T P^T    the score tile's registers are the P^T operand (per page)
 // Masking is applied only to stages that reach past the wave's first query position (the diagonal).
@@ -99,14 +100,16 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   bool bad = false;
 
   const int seq_tokens = ctx + C;
-  constexpr int CPP = NCH / NPG;  // 16-byte chunks per page per thread
-  // Stage `st` = logical pages 4*st .. 4*st+3, copied global -> LDS by the load unit itself
-  // (global_load_lds_dwordx4: each wave instruction lands 64 x 16 B contiguously at its LDS base), so
-  // no registers hold the next stage while the current one computes.  Page ids: four independent
-  // scalar loads, index clamped into the tile's page range so each is in bounds.  A missing or invalid
-  // page is read from page 0 and `patch` zeroes it once the copies have landed, together with the slots
-  // past the end of the sequence in its last page (stale pool contents).
-  auto fetch = [&](int st, int buf, unsigned& okm) {
+  constexpr int CPP = NCH / NPG;  // 16-byte pieces per page per thread
+  // Stage `st` = logical pages 4*st .. 4*st+3.  Piece k of a stage is its bytes [4096k + 1024w, +1024)
+  // for wave w (one page's contiguous kilobyte, 16 bytes per lane).  The next stage's pieces are loaded
+  // into registers at the top of a step and stored to the other LDS buffer at its end, so their
+  // latency hides behind the step's MFMA work; staging through registers measured faster than direct
+  // global->LDS copies.  Page ids: four scalar loads, index clamped into the tile's page range so each
+  // is in bounds.  A missing or invalid page is read from page 0 and `patch` zeroes it once stored,
+  // together with the slots past the end of the sequence in its last page (stale pool contents).
+  u32x4 stg[NCH];
+  auto fetch = [&](int st, unsigned& okm) {
     okm = 0u;
     int ids[NPG];
 #pragma unroll
@@ -119,27 +122,24 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       bad |= inr && !ok;
       ids[pg] = ok ? ids[pg] : 0;
       if constexpr (CPP >= 1) {
-        // wave-uniform page base + a 32-bit lane offset, and a wave-uniform LDS base: the address
-        // arithmetic stays scalar
+        // wave-uniform page base + a 32-bit lane offset
         const unsigned char* pbase = hbase + (int64_t)ids[pg] * page_stride;
 #pragma unroll
-        for (int c = 0; c < CPP; ++c) {
-          const int k = pg * CPP + c;
-          __builtin_amdgcn_global_load_lds(pbase + (uint32_t)(c * 4096 + tid * 16),
-                                           (__attribute__((address_space(3))) void*)(lds + buf * SB + k * 4096 + wvu * 1024),
-                                           16, 0, 0);
-        }
+        for (int c = 0; c < CPP; ++c) stg[pg * CPP + c] = ld16(pbase + (uint32_t)(c * 4096 + tid * 16));
       }
     }
     if constexpr (CPP == 0) {
-      // A page block is smaller than one copy round: round k's wave pieces span 4096 / PB pages.
+      // A page block is smaller than one 4 KB round: round k's wave pieces span 4096 / PB pages.
 #pragma unroll
       for (int k = 0; k < NCH; ++k) {
         const int o = k * 4096 + wvu * 1024;
-        const unsigned char* src = hbase + (int64_t)ids[o / PB] * page_stride + (o % PB) + lane * 16;
-        __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(lds + buf * SB + o), 16, 0, 0);
+        stg[k] = ld16(hbase + (int64_t)ids[o / PB] * page_stride + (uint32_t)((o % PB) + lane * 16));
       }
     }
+  };
+  auto store_stage = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) *reinterpret_cast<u32x4*>(lds + buf * SB + k * 4096 + tid * 16) = stg[k];
   };
   auto patch = [&](int st, int buf, unsigned okm) {
     if ((st + 1) * NPG * 16 <= seq_tokens && okm == (1u << NPG) - 1u) return;
@@ -179,28 +179,42 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     }
   };
   // vmcnt(0): the stage's LDS copies have landed (expcnt / lgkmcnt left unconstrained).
-  auto wait_copies = [] { __builtin_amdgcn_s_waitcnt(0x0F70); };
-
   unsigned okm;  // bit pg: page pg of the stage in flight is valid
-  fetch(0, 0, okm);
-  wait_copies();
+  fetch(0, okm);
+  store_stage(0);
+  // All earlier global loads (the query fragments) have landed: without this, the compiler's waits
+  // for them inside the loop would also wait for each step's staging loads.
+  __builtin_amdgcn_s_waitcnt(0x0F70);
   patch(0, 0, okm);
   __syncthreads();
   int buf = 0;
   for (int st = 0; st < n_stages; ++st) {
     const bool more = st + 1 < n_stages;
-    if (more) fetch(st + 1, buf ^ 1, okm);
+    if (more) fetch(st + 1, okm);
     const unsigned char* sb = lds + buf * SB;
-    // K operand fragments for both 32-key tiles are read from LDS up front, then the two independent
-    // MFMA chains are interleaved; the V fragments are read next so their latency hides behind the
-    // softmax.  Scheduling barriers keep this order.
+    // The two 32-key tiles' MFMA chains are interleaved.  bf16 pages: K operands are read from LDS KD
+    // k-steps ahead of their MFMAs, V operands one page ahead (page 0's before the softmax), which
+    // leaves registers for the staged next stage.  Scheduling barriers keep this order.
     u32x4 kf[2][NS];
+    f32x16 S[2] = {f32x16{}, f32x16{}};
     if constexpr (!FP8) {
+      constexpr int KD = 4;
+      const unsigned char* kp0 = sb + (l32 >> 4) * PB + (g * 16 + (l32 & 15)) * 16;
+      const unsigned char* kp1 = kp0 + 2 * PB;
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const unsigned char* kp = sb + (2 * kk + (l32 >> 4)) * PB + (g * 16 + (l32 & 15)) * 16;
+      for (int s = 0; s < KD; ++s) {
+        kf[0][s] = ld16(kp0 + s * 512);
+        kf[1][s] = ld16(kp1 + s * 512);
+      }
 #pragma unroll
-        for (int s = 0; s < NS; ++s) kf[kk][s] = ld16(kp + s * 512);
+      for (int s = 0; s < NS; ++s) {
+        if (s + KD < NS) {
+          kf[0][s + KD] = ld16(kp0 + (s + KD) * 512);
+          kf[1][s + KD] = ld16(kp1 + (s + KD) * 512);
+        }
+        S[0] = mfma32(kf[0][s], qt[s], S[0]);
+        S[1] = mfma32(kf[1][s], qt[s], S[1]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     } else {
       // piece X = 4P + q (q = g or g + 2) of token t holds k-steps 4P + q/2 (bytes 0-7) and 4P + 2 + q/2
@@ -217,16 +231,17 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
           }
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
-    f32x16 S[2] = {f32x16{}, f32x16{}};
+    if constexpr (FP8) {
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
+      for (int s = 0; s < NS; ++s)
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) S[kk] = mfma32(kf[kk][s], qt[s], S[kk]);
+        for (int kk = 0; kk < 2; ++kk) S[kk] = mfma32(kf[kk][s], qt[s], S[kk]);
+    }
     __builtin_amdgcn_sched_barrier(0);
     u32x4 vf[NPG][NDT];
-#pragma unroll
-    for (int pg = 0; pg < NPG; ++pg) {
+    // V operands: page 0 before the softmax, page pg+1 while page pg's MFMAs run
+    auto load_v = [&](int pg) {
       if constexpr (!FP8) {
         const unsigned char* vp = sb + pg * PB + KBB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 512;
 #pragma unroll
@@ -240,7 +255,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
           vf[pg][d] = cvt8(r.x, r.y);
         }
       }
-    }
+    };
+    load_v(0);
     __builtin_amdgcn_sched_barrier(0);
     // Softmax against a reference max.  With c = scale * log2(e) > 0 (the host rejects other scales),
     // the weights are exp2(c*s - m_run), m_run being the running row max of the earlier stages (exact
@@ -301,11 +317,14 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     l_run += ssum;
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) {
+      if (pg + 1 < NPG) load_v(pg + 1);
 #pragma unroll
       for (int d = 0; d < NDT; ++d) acc[d] = mfma32(vf[pg][d], pb[pg], acc[d]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (more) {
-      wait_copies();
+      store_stage(buf ^ 1);
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), as in the prologue
       patch(st + 1, buf ^ 1, okm);
     }
     __syncthreads();
