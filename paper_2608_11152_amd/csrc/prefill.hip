@@ -94,7 +94,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   const int64_t page_stride = (int64_t)a.Hkv * PB;  // bytes
   const unsigned char* hbase = reinterpret_cast<const unsigned char*>(a.layer) + (int64_t)it.kvh * PB;
   // The block table is read-only for the kernel's lifetime: read it through the constant address space
-  // so page ids are scalar loads (counted apart from the LDS copies, which the compiler must not wait on).
+  // so page ids are scalar loads.
   typedef const __attribute__((address_space(4))) int32_t* const_i32p;
   const_i32p btr = (const_i32p)(a.bt + (int64_t)it.seq * a.maxp);
   bool bad = false;
@@ -178,7 +178,6 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       }
     }
   };
-  // vmcnt(0): the stage's LDS copies have landed (expcnt / lgkmcnt left unconstrained).
   unsigned okm;  // bit pg: page pg of the stage in flight is valid
   fetch(0, okm);
   store_stage(0);
@@ -193,8 +192,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     if (more) fetch(st + 1, okm);
     const unsigned char* sb = lds + buf * SB;
     // The two 32-key tiles' MFMA chains are interleaved.  bf16 pages: K operands are read from LDS KD
-    // k-steps ahead of their MFMAs, V operands one page ahead (page 0's before the softmax), which
-    // leaves registers for the staged next stage.  Scheduling barriers keep this order.
+    // k-steps ahead of their MFMAs (FP8 pages: all of them first, converted), V operands one page ahead
+    // (page 0's before the softmax), which leaves registers for the staged next stage.  Scheduling
+    // barriers keep this order.
     u32x4 kf[2][NS];
     f32x16 S[2] = {f32x16{}, f32x16{}};
     if constexpr (!FP8) {
@@ -230,8 +230,6 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             kf[kk][4 * P + 2 + qh] = cvt8(r[2], r[3]);
           }
       }
-    }
-    if constexpr (FP8) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int s = 0; s < NS; ++s)
@@ -240,7 +238,6 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     }
     __builtin_amdgcn_sched_barrier(0);
     u32x4 vf[NPG][NDT];
-    // V operands: page 0 before the softmax, page pg+1 while page pg's MFMAs run
     auto load_v = [&](int pg) {
       if constexpr (!FP8) {
         const unsigned char* vp = sb + pg * PB + KBB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 512;
@@ -324,7 +321,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     }
     if (more) {
       store_stage(buf ^ 1);
-      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), as in the prologue
+      // vmcnt(0): every staging load has been consumed; stating it lets the compiler drop later waits
+      __builtin_amdgcn_s_waitcnt(0x0F70);
       patch(st + 1, buf ^ 1, okm);
     }
     __syncthreads();
