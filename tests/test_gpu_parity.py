@@ -436,3 +436,102 @@ def test_decode_group_shapes(G, members, d):
                     for i in range(members)])
     assert_close(out, ref, f"group G={G} x{members} d={d}")
     assert_close(out_ng, ref, f"ungrouped G={G} x{members} d={d}")
+
+
+@pytest.mark.parametrize("seed", list(range(11, 23)))
+def test_randomized_batches(seed):
+    """Seeded random batches: groups of 1-12 members with prompts of 0-40 pages (sometimes under one
+    page, so nothing is shared), ungrouped and empty sequences, private tails of 0-3000 tokens, every
+    GQA ratio and both head dims; decode with and without the group hint, and chunked prefill of a few
+    sequences over their own history, against the oracle."""
+    import torch
+    rng = np.random.default_rng(seed)
+    G = int(rng.choice([1, 2, 4, 8, 16]))
+    d = int(rng.choice([64, 128]))
+    Hkv = int(rng.choice([1, 2, 4]))
+    Hq = G * Hkv
+    n_groups = int(rng.integers(1, 5))
+    sizes = rng.integers(1, 13, size=n_groups)
+    n_free = int(rng.integers(0, 5))
+    B = int(sizes.sum()) + n_free
+    group_id = np.concatenate([np.full(int(s), g, np.int32) for g, s in enumerate(sizes)] +
+                              [np.full(n_free, -1, np.int32)])
+    P = rng.integers(0, 641, size=n_groups)          # prompt tokens per group
+    shared = (P // 16).astype(np.int32)
+    priv = rng.integers(0, 3001, size=B)
+    priv[rng.random(B) < 0.1] = 0                    # some members have no private tokens (or none at all)
+    lens = np.array([(P[group_id[i]] if group_id[i] >= 0 else 0) + priv[i] for i in range(B)], np.int32)
+    pages = [(int(n) + 15) // 16 for n in lens]
+    num_pages = int(shared.sum()) + sum(pages) + 5
+    perm = rng.permutation(num_pages).astype(np.int32)
+    maxp = max(1, max(pages))
+    bt = np.full((B, maxp), -1, np.int32)
+    nxt = 0
+    gpages = []
+    for g in range(n_groups):
+        gpages.append(perm[nxt:nxt + shared[g]])
+        nxt += shared[g]
+    toks = []
+    prompts = [W.f32_to_bf16_bits(rng.standard_normal((int(P[g]), 2, Hkv, d), dtype=np.float32))
+               for g in range(n_groups)]
+    for i in range(B):
+        g = group_id[i]
+        S = int(shared[g]) if g >= 0 and lens[i] > 0 else 0
+        bt[i, :S] = gpages[g][:S] if S else bt[i, :S]
+        k = pages[i] - S
+        bt[i, S:S + k] = perm[nxt:nxt + k]
+        nxt += k
+        own = W.f32_to_bf16_bits(rng.standard_normal((int(priv[i]), 2, Hkv, d), dtype=np.float32))
+        full = np.concatenate([prompts[g], own]) if g >= 0 else own
+        toks.append(full[:lens[i]])
+    pool = kp.Pool(1, num_pages, Hkv, d)
+    btd = torch.from_numpy(bt).cuda()
+    note(f"randomized batch seed={seed} G={G} d={d} Hkv={Hkv} B={B} groups={n_groups}")
+    # shared prompt pages are written once, by each group's first decoding member
+    first = {}
+    for i in range(B):
+        g = group_id[i]
+        if g >= 0 and lens[i] > 0 and g not in first:
+            first[g] = i
+    cnt0 = np.zeros(B, np.int64)
+    src0 = []
+    for g, i in first.items():
+        cnt0[i] = shared[g] * 16
+        src0.append(toks[i][:shared[g] * 16])
+    gp = kp.group_prefix(group_id, shared)
+    if cnt0.sum():
+        order = sorted(first.values())
+        kv0 = to_dev_bits(np.concatenate([toks[i][:cnt0[i]] for i in order]))
+        kp.kv_append(pool, 0, kv0[:, 0].contiguous(), kv0[:, 1].contiguous(), btd, np.zeros(B, np.int32),
+                     np.concatenate([[0], np.cumsum(cnt0)]).astype(np.int32))
+    start = np.array([shared[group_id[i]] * 16 if group_id[i] >= 0 and lens[i] > 0 else 0 for i in range(B)],
+                     np.int32)
+    rest = [toks[i][start[i]:] for i in range(B)]
+    cu = np.concatenate([[0], np.cumsum([len(r) for r in rest])]).astype(np.int32)
+    if cu[-1]:
+        kv1 = to_dev_bits(np.concatenate([r for r in rest if len(r)]))
+        kp.kv_append(pool, 0, kv1[:, 0].contiguous(), kv1[:, 1].contiguous(), btd, start, cu, group_prefix=gp)
+    qb = W.f32_to_bf16_bits(rng.standard_normal((B, Hq, d), dtype=np.float32))
+    out = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, lens, group_prefix=gp, scale=0.1)
+    out_ng = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, lens, scale=0.1)
+    torch.cuda.synchronize()
+    assert pool.device_error() == kp.KVP_OK
+    ref = np.stack([oracle.decode_seq(qb[i], oracle.widen_bf16(toks[i][:, 0]), oracle.widen_bf16(toks[i][:, 1]), 0.1)
+                    if lens[i] else np.zeros((Hq, d)) for i in range(B)])
+    assert_close(out, ref, f"randomized decode seed={seed}")
+    assert_close(out_ng, ref, f"randomized decode (no hint) seed={seed}")
+    # chunked prefill: the last C tokens of a few sequences as the chunk over the rest as history
+    sel = [i for i in range(B) if lens[i] >= 2][:3]
+    if not sel:
+        return
+    C = [int(rng.integers(1, min(int(lens[i]), 300) + 1)) for i in sel]
+    ctx = [int(lens[i]) - c for i, c in zip(sel, C)]
+    cu_q = np.concatenate([[0], np.cumsum(C)]).astype(np.int32)
+    qp = W.f32_to_bf16_bits(rng.standard_normal((int(cu_q[-1]), Hq, d), dtype=np.float32))
+    btp = torch.from_numpy(np.ascontiguousarray(bt[sel])).cuda()
+    outp = kp.prefix_chunk_prefill_attn(to_dev_bits(qp), pool, 0, btp, ctx, cu_q, scale=0.1)
+    torch.cuda.synchronize()
+    refp = np.concatenate([oracle.prefill_seq(qp[cu_q[j]:cu_q[j + 1]], oracle.widen_bf16(toks[i][:, 0]),
+                                              oracle.widen_bf16(toks[i][:, 1]), 0.1, ctx[j])
+                           for j, i in enumerate(sel)])
+    assert_close(outp, refp, f"randomized prefill seed={seed}")
