@@ -36,9 +36,9 @@ __device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// FP8 pages (FP8 = true): a stage holds half the bytes; every 16-byte K piece read from LDS carries the
-// operands of two k-steps and every V operand is an 8-byte read, both converted exactly to bf16 in
-// registers.  The K scale is folded into the score scale and the V scale into the output.
+// FP8 pages (FP8 = true): a stage moves half the bytes from the pool and is converted exactly to bf16
+// once, on its way into LDS; the matrix-core loop is the bf16 one.  The K scale is folded into the score
+// scale and the V scale into the output.
 __device__ __forceinline__ unsigned cvt_fp8x2(unsigned w, bool hi) {
   return __builtin_bit_cast(unsigned, hi ? __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, true)
                                          : __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false));
@@ -53,11 +53,12 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   constexpr int NS = D / 16;           // k-steps of the score product
   constexpr int NDT = D / 32;          // 32-row d tiles of the output
   constexpr int KB = 16 * D;           // elements per K (or V) block
-  constexpr int KBB = FP8 ? KB : 2 * KB;  // bytes per K (or V) block
-  constexpr int PB = 2 * KBB;          // bytes per (page, head) block
+  constexpr int KBB = 2 * KB;          // bytes per bf16 K (or V) block: the LDS stages are always bf16
+  constexpr int PB = 2 * KBB;          // bytes per (page, head) block in LDS
+  constexpr int PBG = FP8 ? 2 * KB : PB;  // bytes per (page, head) block in the pool
   constexpr int NPG = 4;               // pages per stage
-  constexpr int SB = NPG * PB;
-  constexpr int NCH = SB / (256 * 16);
+  constexpr int SB = NPG * PB;         // bytes per LDS stage
+  constexpr int NCH = NPG * PBG / (256 * 16);  // 16-byte pool pieces per thread per stage
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * SB];
 
   const PrefillItem it = a.items[blockIdx.x];
@@ -91,8 +92,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   float m_run = -INFINITY, l_run = 0.0f;
   const float cs = a.scale_log2;
 
-  const int64_t page_stride = (int64_t)a.Hkv * PB;  // bytes
-  const unsigned char* hbase = reinterpret_cast<const unsigned char*>(a.layer) + (int64_t)it.kvh * PB;
+  const int64_t page_stride = (int64_t)a.Hkv * PBG;  // bytes
+  const unsigned char* hbase = reinterpret_cast<const unsigned char*>(a.layer) + (int64_t)it.kvh * PBG;
   // The block table is read-only for the kernel's lifetime: read it through the constant address space
   // so page ids are scalar loads.
   typedef const __attribute__((address_space(4))) int32_t* const_i32p;
@@ -100,7 +101,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   bool bad = false;
 
   const int seq_tokens = ctx + C;
-  constexpr int CPP = NCH / NPG;  // 16-byte pieces per page per thread
+  constexpr int CPP = NCH / NPG;  // 16-byte pool pieces per page per thread
   // Stage `st` = logical pages 4*st .. 4*st+3.  Piece k of a stage is its bytes [4096k + 1024w, +1024)
   // for wave w (one page's contiguous kilobyte, 16 bytes per lane).  The next stage's pieces are loaded
   // into registers at the top of a step and stored to the other LDS buffer at its end, so their
@@ -129,19 +130,66 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       }
     }
     if constexpr (CPP == 0) {
-      // A page block is smaller than one 4 KB round: round k's wave pieces span 4096 / PB pages.
+      // A page block is smaller than one 4 KB round: round k's wave pieces span 4096 / PBG pages.
 #pragma unroll
       for (int k = 0; k < NCH; ++k) {
         const int o = k * 4096 + wvu * 1024;
-        stg[k] = ld16(hbase + (int64_t)ids[o / PB] * page_stride + (uint32_t)((o % PB) + lane * 16));
+        stg[k] = ld16(hbase + (int64_t)ids[o / PBG] * page_stride + (uint32_t)((o % PBG) + lane * 16));
       }
     }
   };
-  auto store_stage = [&](int buf) {
+  // bf16 pools: the pieces go to LDS as they are.  FP8 pools: each 16-byte piece is converted (exactly)
+  // into the two 16-byte bf16 rows it holds (a K piece: two 8-dim chunks of one token; a V piece: 8
+  // slots of two dims), so the LDS stage has the bf16 layout and the MFMA loop is shared.  Tokens past
+  // the sequence end and pages that are missing or invalid are zeroed here, in registers.
+  auto store_stage = [&](int st, int buf, unsigned okm) {
+    if constexpr (!FP8) {
 #pragma unroll
-    for (int k = 0; k < NCH; ++k) *reinterpret_cast<u32x4*>(lds + buf * SB + k * 4096 + tid * 16) = stg[k];
+      for (int k = 0; k < NCH; ++k) *reinterpret_cast<u32x4*>(lds + buf * SB + k * 4096 + tid * 16) = stg[k];
+    } else {
+      const bool whole = (st + 1) * NPG * 16 <= seq_tokens && okm == (1u << NPG) - 1u;
+#pragma unroll
+      for (int k = 0; k < NCH; ++k) {
+        const int o = k * 4096 + wvu * 1024;
+        const int pg = o / PBG;
+        const int ob = (o % PBG) + lane * 16;  // byte of the piece in its (page, head) block
+        u32x4 lo = cvt8(stg[k][0], stg[k][1]), hi = cvt8(stg[k][2], stg[k][3]);
+        int dlo, dhi;
+        if (ob < KB) {
+          const int X = ob >> 8, t = (ob >> 4) & 15;  // piece X of token t
+          const int ca = 8 * (X >> 2) + (X & 3);     // its 8-dim chunks ca and ca + 4
+          dlo = (ca * 16 + t) * 16;
+          dhi = ((ca + 4) * 16 + t) * 16;
+          if (!whole) {
+            const int valid = (okm >> pg) & 1u ? seq_tokens - (st * NPG + pg) * 16 : 0;
+            if (t >= valid) lo = hi = u32x4{0u, 0u, 0u, 0u};
+          }
+        } else {
+          const int vp = (ob - KB) >> 4;
+          const int Y = vp >> 5, sh = (vp >> 4) & 1, c16 = vp & 15;  // slots 8sh.. of dims 32Y+c16, +16
+          dlo = KBB + ((4 * Y + sh) * 16 + c16) * 16;
+          dhi = KBB + ((4 * Y + 2 + sh) * 16 + c16) * 16;
+          if (!whole) {
+            const int valid = (okm >> pg) & 1u ? seq_tokens - (st * NPG + pg) * 16 : 0;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              const unsigned m = (slot_token(8 * sh + 2 * w) < valid ? 0xFFFFu : 0u) |
+                                 (slot_token(8 * sh + 2 * w + 1) < valid ? 0xFFFF0000u : 0u);
+              lo[w] &= m;
+              hi[w] &= m;
+            }
+          }
+        }
+        unsigned char* dst = lds + buf * SB + pg * PB;
+        *reinterpret_cast<u32x4*>(dst + dlo) = lo;
+        *reinterpret_cast<u32x4*>(dst + dhi) = hi;
+      }
+    }
   };
+  // bf16 pools: zero, in this thread's own pieces of stage st, the pages that are missing or invalid and
+  // the slots past the end of the sequence (stale pool contents), after they are stored.
   auto patch = [&](int st, int buf, unsigned okm) {
+    if constexpr (FP8) return;  // masked on the way to LDS
     if ((st + 1) * NPG * 16 <= seq_tokens && okm == (1u << NPG) - 1u) return;
     // Piece k of this thread: stage bytes [4096k + 16 tid, +16), in page (4096k + 1024 wv) / PB.
 #pragma unroll
@@ -150,37 +198,26 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       const int pg = o / PB;
       const int valid = (okm >> pg) & 1u ? seq_tokens - (st * NPG + pg) * 16 : 0;  // usable tokens of this page
       if (valid >= 16) continue;
-      {
-        const int inb = (o % PB) + lane * 16;
-        u32x4* lp = reinterpret_cast<u32x4*>(lds + buf * SB + o + lane * 16);
-        u32x4 v = *lp;
-        if (inb < KBB) {
-          if (((inb >> 4) & 15) >= valid) v = u32x4{0u, 0u, 0u, 0u};
-        } else if (!FP8) {
-          const int h = ((inb - KBB) >> 8) & 1;  // V chunk holds slots 8h..8h+7
+      const int inb = (o % PB) + lane * 16;
+      u32x4* lp = reinterpret_cast<u32x4*>(lds + buf * SB + o + lane * 16);
+      u32x4 v = *lp;
+      if (inb < KBB) {
+        if (((inb >> 4) & 15) >= valid) v = u32x4{0u, 0u, 0u, 0u};
+      } else {
+        const int h = ((inb - KBB) >> 8) & 1;  // V chunk holds slots 8h..8h+7
 #pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const unsigned lo = slot_token(8 * h + 2 * w) < valid ? 0xFFFFu : 0u;
-            const unsigned hi = slot_token(8 * h + 2 * w + 1) < valid ? 0xFFFF0000u : 0u;
-            v[w] &= lo | hi;
-          }
-        } else {
-          const int h = ((inb - KBB) >> 8) & 1;  // V piece holds slots 8h..8h+7 of two d-tiles
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            unsigned m = 0u;
-#pragma unroll
-            for (int b = 0; b < 4; ++b) m |= (slot_token(8 * h + ((4 * w + b) & 7)) < valid ? 0xFFu : 0u) << (8 * b);
-            v[w] &= m;
-          }
+        for (int w = 0; w < 4; ++w) {
+          const unsigned lo = slot_token(8 * h + 2 * w) < valid ? 0xFFFFu : 0u;
+          const unsigned hi = slot_token(8 * h + 2 * w + 1) < valid ? 0xFFFF0000u : 0u;
+          v[w] &= lo | hi;
         }
-        *lp = v;
       }
+      *lp = v;
     }
   };
   unsigned okm;  // bit pg: page pg of the stage in flight is valid
   fetch(0, okm);
-  store_stage(0);
+  store_stage(0, 0, okm);
   // All earlier global loads (the query fragments) have landed: without this, the compiler's waits
   // for them inside the loop would also wait for each step's staging loads.
   __builtin_amdgcn_s_waitcnt(0x0F70);
@@ -191,67 +228,37 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     const bool more = st + 1 < n_stages;
     if (more) fetch(st + 1, okm);
     const unsigned char* sb = lds + buf * SB;
-    // The two 32-key tiles' MFMA chains are interleaved.  bf16 pages: K operands are read from LDS KD
-    // k-steps ahead of their MFMAs (FP8 pages: all of them first, converted), V operands one page ahead
-    // (page 0's before the softmax), which leaves registers for the staged next stage.  Scheduling
-    // barriers keep this order.
-    u32x4 kf[2][NS];
+    // The two 32-key tiles' MFMA chains are interleaved.  K operands are read from LDS KD k-steps ahead
+    // of their MFMAs, V operands one page ahead (page 0's before the softmax), which leaves registers for
+    // the staged next stage.  Scheduling barriers keep this order.
     f32x16 S[2] = {f32x16{}, f32x16{}};
-    if constexpr (!FP8) {
+    {
       constexpr int KD = 4;
       const unsigned char* kp0 = sb + (l32 >> 4) * PB + (g * 16 + (l32 & 15)) * 16;
       const unsigned char* kp1 = kp0 + 2 * PB;
+      u32x4 k0[NS], k1[NS];
 #pragma unroll
       for (int s = 0; s < KD; ++s) {
-        kf[0][s] = ld16(kp0 + s * 512);
-        kf[1][s] = ld16(kp1 + s * 512);
+        k0[s] = ld16(kp0 + s * 512);
+        k1[s] = ld16(kp1 + s * 512);
       }
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         if (s + KD < NS) {
-          kf[0][s + KD] = ld16(kp0 + (s + KD) * 512);
-          kf[1][s + KD] = ld16(kp1 + (s + KD) * 512);
+          k0[s + KD] = ld16(kp0 + (s + KD) * 512);
+          k1[s + KD] = ld16(kp1 + (s + KD) * 512);
         }
-        S[0] = mfma32(kf[0][s], qt[s], S[0]);
-        S[1] = mfma32(kf[1][s], qt[s], S[1]);
+        S[0] = mfma32(k0[s], qt[s], S[0]);
+        S[1] = mfma32(k1[s], qt[s], S[1]);
         __builtin_amdgcn_sched_barrier(0);
       }
-    } else {
-      // piece X = 4P + q (q = g or g + 2) of token t holds k-steps 4P + q/2 (bytes 0-7) and 4P + 2 + q/2
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const unsigned char* kp = sb + (2 * kk + (l32 >> 4)) * PB + (l32 & 15) * 16;
-#pragma unroll
-        for (int P = 0; P < D / 64; ++P)
-#pragma unroll
-          for (int qh = 0; qh < 2; ++qh) {
-            const u32x4 r = ld16(kp + ((4 * P + g + 2 * qh) * 16) * 16);
-            kf[kk][4 * P + qh] = cvt8(r[0], r[1]);
-            kf[kk][4 * P + 2 + qh] = cvt8(r[2], r[3]);
-          }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int s = 0; s < NS; ++s)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) S[kk] = mfma32(kf[kk][s], qt[s], S[kk]);
     }
     __builtin_amdgcn_sched_barrier(0);
     u32x4 vf[NPG][NDT];
     auto load_v = [&](int pg) {
-      if constexpr (!FP8) {
-        const unsigned char* vp = sb + pg * PB + KBB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 512;
+      const unsigned char* vp = sb + pg * PB + KBB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 512;
 #pragma unroll
-        for (int d = 0; d < NDT; ++d) vf[pg][d] = ld16(vp + d * 1024);
-      } else {
-        // piece (Y = d, h = g, dim l32 % 16): bytes 8 (l32 / 16) .. +7 are this lane's 8 slots
-        const unsigned char* vp = sb + pg * PB + KBB + (g * 16 + (l32 & 15)) * 16 + (l32 >> 4) * 8;
-#pragma unroll
-        for (int d = 0; d < NDT; ++d) {
-          const uint2 r = *reinterpret_cast<const uint2*>(vp + d * 512);
-          vf[pg][d] = cvt8(r.x, r.y);
-        }
-      }
+      for (int d = 0; d < NDT; ++d) vf[pg][d] = ld16(vp + d * 1024);
     };
     load_v(0);
     __builtin_amdgcn_sched_barrier(0);
@@ -320,7 +327,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       __builtin_amdgcn_sched_barrier(0);
     }
     if (more) {
-      store_stage(buf ^ 1);
+      store_stage(st + 1, buf ^ 1, okm);
       // vmcnt(0): every staging load has been consumed; stating it lets the compiler drop later waits
       __builtin_amdgcn_s_waitcnt(0x0F70);
       patch(st + 1, buf ^ 1, okm);
