@@ -386,8 +386,9 @@ int kv_pool_create(kvp_pool_t* out, int num_layers, int num_pages, int page_size
   hipError_t e = hipGetDevice(&p->device);
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&p->base), p->layer_bytes * num_layers);
   if (e != hipSuccess) {
+    const size_t want = p->layer_bytes * num_layers;
     delete p;
-    return set_err(KVP_ENOMEM, "hipMalloc(pool of %zu bytes): %s", (size_t)0, hipGetErrorString(e));
+    return set_err(KVP_ENOMEM, "hipMalloc(pool of %zu bytes): %s", want, hipGetErrorString(e));
   }
   e = hipMalloc(reinterpret_cast<void**>(&p->err), 256);
   if (e == hipSuccess) e = kvp::launch_fill_zero(p->base, p->layer_bytes * num_layers, nullptr);

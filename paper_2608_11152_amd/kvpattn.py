@@ -143,6 +143,42 @@ def _dptr(t) -> C.c_void_p:
     return C.c_void_p(t.data_ptr() if t is not None else 0)
 
 
+def _dev(t, name: str, dtypes, ndim: int | None = None, rows: int | None = None, tail=None):
+    """The library receives device tensors as bare pointers laid out as the header states (dense, row
+    major).  Check here what those pointers are assumed to hold, before anything is launched: on the GPU,
+    dense, of the expected dtype and rank, with at least `rows` rows and trailing dimensions `tail`."""
+    if t is None:
+        raise ValueError(f"{name} is None")
+    if not getattr(t, "is_cuda", False):
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}; expected one of {', '.join(str(d) for d in dtypes)}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} has {t.dim()} dimensions, expected {ndim}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if rows is not None and t.shape[0] < rows:
+        raise ValueError(f"{name} has {t.shape[0]} rows, {rows} needed")
+    if tail is not None and tuple(t.shape[1:]) != tuple(tail):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected (*, {', '.join(map(str, tail))})")
+    return t
+
+
+def _bf16():
+    import torch
+    return (torch.bfloat16,)
+
+
+def _i32t():
+    import torch
+    return (torch.int32,)
+
+
+def _outt():
+    import torch
+    return (torch.float32, torch.bfloat16)
+
+
 class Pool:
     """A paged KV pool owned by the library (kv_pool_create / kv_pool_destroy)."""
 
@@ -227,6 +263,13 @@ def kv_pool_device_error(pool: Pool) -> int:
 def kv_append(pool: Pool, layer, k, v, block_tables, start_pos, cu_new, group_prefix=None, stream=None):
     """k, v: device bf16 [T, Hkv, d]; block_tables: device int32 [B, maxp]; start_pos, cu_new: host."""
     sp, cu = _i32(start_pos), _i32(cu_new)
+    if len(cu) != len(sp) + 1:
+        raise ValueError(f"cu_new has {len(cu)} entries, {len(sp) + 1} needed")
+    _dev(block_tables, "block_tables", _i32t(), 2, rows=len(sp))
+    if len(sp) and int(cu[-1]) > 0:
+        tail = (pool.num_kv_heads, pool.head_dim)
+        _dev(k, "k", _bf16(), 3, rows=int(cu[-1]), tail=tail)
+        _dev(v, "v", _bf16(), 3, rows=int(cu[-1]), tail=tail)
     _check(lib().kv_append(pool.handle, layer, _dptr(k), _dptr(v), _dptr(block_tables), block_tables.shape[1],
                            _ptr(sp), _ptr(cu), len(sp), _gp_ref(group_prefix), _stream(stream)), "kv_append")
 
@@ -234,6 +277,7 @@ def kv_append(pool: Pool, layer, k, v, block_tables, start_pos, cu_new, group_pr
 def kv_gather(pool: Pool, layer, block_tables, lens, stream=None):
     import torch
     ln = _i32(lens)
+    _dev(block_tables, "block_tables", _i32t(), 2, rows=len(ln))
     T = int(ln.sum())
     shape = (T, pool.num_kv_heads, pool.head_dim)
     k = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
@@ -256,18 +300,24 @@ def paged_decode_attn(q, pool: Pool, layer, block_tables, seq_lens, group_prefix
     """q: device bf16 [B, Hq, d]; block_tables: device int32 [B, maxp]; seq_lens: host int32 [B]."""
     import torch
     sl = _i32(seq_lens)
+    _dev(q, "q", _bf16(), 3)
     B, Hq, d = q.shape
+    if B != len(sl):
+        raise ValueError(f"q holds {B} sequences, seq_lens {len(sl)}")
+    _dev(block_tables, "block_tables", _i32t(), 2, rows=B)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     if out is None:
         out = torch.empty((B, Hq, d), dtype=out_dtype or torch.float32, device=q.device)
+    _dev(out, "out", _outt(), 3, rows=B, tail=(Hq, d))
     od = KVP_F32 if out.dtype == torch.float32 else KVP_BF16
     gpr = group_prefix if not isinstance(group_prefix, tuple) else _GP(*group_prefix)
     if ws is None:
         ws = torch.empty(max(1, paged_decode_workspace_size(pool, sl, Hq, gpr)), dtype=torch.uint8, device=q.device)
+    _dev(ws, "ws", (ws.dtype,))
     _check(lib().paged_decode_attn(_dptr(q), pool.handle, layer, _dptr(block_tables), block_tables.shape[1],
                                    _ptr(sl), len(sl), _gp_ref(gpr), Hq, float(scale), _dptr(out), od, _dptr(ws),
-                                   ws.numel(), _stream(stream)), "paged_decode_attn")
+                                   ws.numel() * ws.element_size(), _stream(stream)), "paged_decode_attn")
     return out
 
 
@@ -284,18 +334,26 @@ def prefix_chunk_prefill_attn(q, pool: Pool, layer, block_tables, ctx_lens, cu_q
     """q: device bf16 [sum C, Hq, d]; block_tables: device int32 [B, maxp]; ctx_lens, cu_q: host."""
     import torch
     cl, cq = _i32(ctx_lens), _i32(cu_q)
+    if len(cq) != len(cl) + 1:
+        raise ValueError(f"cu_q has {len(cq)} entries, {len(cl) + 1} needed")
+    _dev(q, "q", _bf16(), 3)
     T, Hq, d = q.shape
+    if len(cl) and T != int(cq[-1]):
+        raise ValueError(f"q holds {T} rows, cu_q ends at {int(cq[-1])}")
+    _dev(block_tables, "block_tables", _i32t(), 2, rows=len(cl))
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     if out is None:
         out = torch.empty((T, Hq, d), dtype=out_dtype or torch.float32, device=q.device)
+    _dev(out, "out", _outt(), 3, rows=T, tail=(Hq, d))
     od = KVP_F32 if out.dtype == torch.float32 else KVP_BF16
     if ws is None:
         ws = torch.empty(max(1, prefix_chunk_prefill_workspace_size(pool, cl, cq, Hq)), dtype=torch.uint8,
                          device=q.device)
+    _dev(ws, "ws", (ws.dtype,))
     _check(lib().prefix_chunk_prefill_attn(_dptr(q), pool.handle, layer, _dptr(block_tables), block_tables.shape[1],
                                            _ptr(cl), _ptr(cq), len(cl), Hq, float(scale), _dptr(out), od, _dptr(ws),
-                                           ws.numel(), _stream(stream)), "prefix_chunk_prefill_attn")
+                                           ws.numel() * ws.element_size(), _stream(stream)), "prefix_chunk_prefill_attn")
     return out
 
 

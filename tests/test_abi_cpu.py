@@ -170,3 +170,19 @@ def test_pool_create_rejects_unsupported_shapes_without_a_device():
     assert L.kv_pool_create(ctypes.byref(h), 0, 16, 16, 2, 128, 0) == kp.KVP_EINVAL
     assert L.kv_pool_create(None, 1, 16, 16, 2, 128, 0) == kp.KVP_EINVAL
     assert L.kv_pool_destroy(None) == kp.KVP_OK
+
+
+def test_binding_refuses_host_tensors():
+    """Device arguments are bare pointers to the library: the binding refuses host tensors up front (this
+    runs without a GPU; nothing reaches the library)."""
+    import torch
+    q = torch.zeros((2, 8, 64), dtype=torch.bfloat16)
+    bt = torch.zeros((2, 4), dtype=torch.int32)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        kp.paged_decode_attn(q, None, 0, bt, [16, 16])
+    with pytest.raises(ValueError, match="GPU tensor"):
+        kp.prefix_chunk_prefill_attn(q, None, 0, bt, [0, 0], [0, 1, 2])
+    with pytest.raises(ValueError, match="cu_new"):
+        kp.kv_append(None, 0, q, q, bt, [0, 0], [0, 1])
+    with pytest.raises(ValueError, match="GPU tensor"):
+        kp.kv_append(None, 0, q, q, bt, [0, 0], [0, 1, 2])

@@ -348,6 +348,52 @@ def test_host_errors_enqueue_nothing(cases):
     assert e.value.code == kp.KVP_ESHARED
 
 
+def test_binding_checks_tensors_before_launch(cases):
+    """The C-ABI takes bare device pointers, so the binding checks what they are assumed to hold (dtype,
+    rank, density, row counts) and raises before anything is enqueued."""
+    import torch
+    c = get_case(cases, "tiny")
+    w = c.w
+    q = to_dev_bits(c.vals.q)
+    lens = w.decode_len
+    sentinel = torch.full((w.B, w.Hq, w.d), 7.0, device="cuda")
+    bad_calls = {
+        "q with one sequence fewer": lambda: kp.paged_decode_attn(q[:-1].contiguous(), c.pool, 0, c.bt, lens,
+                                                                 out=sentinel),
+        "q in float32": lambda: kp.paged_decode_attn(q.float(), c.pool, 0, c.bt, lens, out=sentinel),
+        "strided q": lambda: kp.paged_decode_attn(q.transpose(0, 1).contiguous().transpose(0, 1), c.pool, 0,
+                                                  c.bt, lens, out=sentinel),
+        "block tables of int64": lambda: kp.paged_decode_attn(q, c.pool, 0, c.bt.long(), lens, out=sentinel),
+        "block tables missing a row": lambda: kp.paged_decode_attn(q, c.pool, 0, c.bt[:-1], lens, out=sentinel),
+        "column slice of the block tables": lambda: kp.paged_decode_attn(q, c.pool, 0, c.bt[:, :-1], lens,
+                                                                         out=sentinel),
+        "out of the wrong shape": lambda: kp.paged_decode_attn(q, c.pool, 0, c.bt, lens, out=sentinel[:, :-1]),
+        "out in float16": lambda: kp.paged_decode_attn(q, c.pool, 0, c.bt, lens, out=sentinel.half()),
+        "host q": lambda: kp.paged_decode_attn(q.cpu(), c.pool, 0, c.bt, lens, out=sentinel),
+    }
+    for what, call in bad_calls.items():
+        note(f"binding check: {what}")
+        with pytest.raises(ValueError):
+            call()
+    kv = c.kv_dev
+    sp = np.zeros(w.B, np.int32)
+    cu = np.arange(w.B + 1, dtype=np.int32)
+    k1, v1 = kv[: w.B - 1, 0].contiguous(), kv[: w.B - 1, 1].contiguous()
+    note("binding check: kv_append with fewer token rows than cu_new")
+    with pytest.raises(ValueError):
+        kp.kv_append(c.pool, 0, k1, v1, c.bt, sp, cu)
+    note("binding check: kv_append with a wrong head count")
+    with pytest.raises(ValueError):
+        kp.kv_append(c.pool, 0, kv[: w.B, 0, :1].contiguous(), kv[: w.B, 1, :1].contiguous(), c.bt, sp, cu)
+    cq = np.array([0, 3], np.int32)
+    qp = torch.zeros((4, w.Hq, w.d), dtype=torch.bfloat16, device="cuda")
+    note("binding check: prefill q rows differ from cu_q")
+    with pytest.raises(ValueError):
+        kp.prefix_chunk_prefill_attn(qp, c.pool, 0, c.bt, np.array([0], np.int32), cq)
+    torch.cuda.synchronize()
+    assert torch.all(sentinel == 7.0)
+
+
 def test_bad_page_id_is_skipped_and_reported():
     """An out-of-pool page id in a device block table is never dereferenced: the kernels skip the page and
     record KVP_ERANGE; outputs stay finite and equal attention over the remaining pages."""
