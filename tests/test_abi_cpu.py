@@ -130,6 +130,22 @@ def test_plan_large_group_splits_into_subgroups():
     assert len(pref) == 3 and set(pref[:, 6].tolist()) == {8}
 
 
+def test_plan_wide_group_goes_to_waves_only_when_prefix_is_small():
+    """A group wider than one wave (8 members x 8 heads) is read per 16-column subgroup on the wave path
+    when that adds at most 1% pages to the call; otherwise it stays one LDS-staged item per page range."""
+    G, B = 8, 8
+    long_private = [2 * 16 + 4000] * B  # 2 shared pages, ~250 private pages each: 6 extra pages of ~2000
+    items, _, _ = _coverage(long_private, np.zeros(B, np.int32), np.array([2], np.int32), Hq=32, Hkv=4)
+    pref = items[items[:, 0] == 1]
+    assert len(pref) > 0 and np.all(pref[:, 6] * G <= 16)
+    assert sorted(set(pref[:, 6].tolist())) == [2]  # four subgroups of two members, each reads the prefix
+    assert int((pref[:, 3] - pref[:, 2]).sum()) == 4 * 2
+    long_prefix = [40 * 16 + 100] * B  # 40 shared pages against ~7 private pages each
+    items, _, _ = _coverage(long_prefix, np.zeros(B, np.int32), np.array([40], np.int32), Hq=32, Hkv=4)
+    pref = items[items[:, 0] == 1]
+    assert np.all(pref[:, 6] == B) and int((pref[:, 3] - pref[:, 2]).sum()) == 40
+
+
 def test_plan_validation_codes():
     with pytest.raises(kp.KvpError) as e:
         kp.kvp_plan_decode([10], 12, 4)  # G = 3

@@ -435,13 +435,30 @@ def test_pool_reset_zeroes(cases):
 def test_decode_group_shapes(G, members, d):
     """Shared-prefix groups of every tiling: 2 and 3 column tiles on the LDS path, subgroups (> 64
     columns, with a remainder small enough for the wave path), G = 1 and G = 16, odd member counts."""
+    rng = np.random.default_rng(G * 100 + members + d)
+    P = int(rng.integers(40, 300))           # prompt tokens; shared whole pages = P // 16
+    priv = rng.integers(1, 500, size=members)
+    _run_group_case(G, members, d, P, priv, rng, "group shapes")
+
+
+@pytest.mark.parametrize("G,members,d", [(8, 8, 128), (4, 12, 64), (16, 3, 128), (2, 40, 128)])
+def test_decode_wide_group_on_wave_path(G, members, d):
+    """A wide group whose prompt is a small share of the call's pages is planned as 16-column wave items
+    (the prompt pages read once per subgroup, the call launched wave-only): same results."""
+    rng = np.random.default_rng(700 + G * 10 + members)
+    P = int(rng.integers(32, 60))
+    priv = rng.integers(3000, 4000, size=members)
+    gp = kp.group_prefix(np.zeros(members, np.int32), np.array([P // 16], np.int32))
+    items, _, _ = kp.kvp_plan_decode((P + priv).astype(np.int32), G * 2, 2, gp)
+    assert np.all(items[:, 6] * G <= 16), "expected a wave-only plan"
+    _run_group_case(G, members, d, P, priv, rng, "wide group on waves")
+
+
+def _run_group_case(G, members, d, P, priv, rng, tag):
     import torch
     Hkv = 2
     Hq = G * Hkv
-    rng = np.random.default_rng(G * 100 + members + d)
-    P = int(rng.integers(40, 300))           # prompt tokens; shared whole pages = P // 16
     S = P // 16
-    priv = rng.integers(1, 500, size=members)
     lens = (P + priv).astype(np.int32)
     pages = [(int(n) + 15) // 16 for n in lens]
     num_pages = S + sum(p - S for p in pages) + 7
@@ -460,7 +477,7 @@ def test_decode_group_shapes(G, members, d):
     qb = W.f32_to_bf16_bits(rng.standard_normal((members, Hq, d), dtype=np.float32))
     pool = kp.Pool(1, num_pages, Hkv, d)
     btd = torch.from_numpy(bt).cuda()
-    note(f"group shapes G={G} members={members} d={d} P={P}")
+    note(f"{tag} G={G} members={members} d={d} P={P}")
     # the first member writes the shared prompt pages, then every member writes its tail + private tokens
     cnt0 = np.zeros(members, np.int64)
     cnt0[0] = S * 16
