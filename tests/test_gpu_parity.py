@@ -133,6 +133,48 @@ def test_decode_deterministic(cases):
     assert torch.equal(c.decode(), c.decode())
 
 
+def test_many_calls_in_flight_on_two_streams(cases):
+    """Two dozen decode and prefill calls queued on two streams with no host synchronisation in between,
+    more than the library's pinned metadata slots (a slot is reused only after the GPU work that read it
+    has completed). Each call has its own lengths, so a slot handed out too early would show: every
+    output must equal the same call made alone."""
+    import torch
+    c = get_case(cases, "mixed_s")
+    w = c.w
+    q, qp = to_dev_bits(c.vals.q), to_dev_bits(c.vals.qp)
+    s0, s1 = int(w.prefill_seqs[0]), int(w.prefill_seqs[-1]) + 1
+    floor = np.zeros(w.B, np.int64)
+    if w.num_groups:
+        grouped = w.group_id >= 0
+        floor[grouped] = w.shared_pages[w.group_id[grouped]] * 16
+    variants = []
+    for k in range(4):
+        lens = np.maximum(w.decode_len - 5 * k, np.minimum(w.decode_len, floor + 1)).astype(np.int32)
+        variants.append(("decode", lens, c.gp if k % 2 == 0 else None))
+    variants.append(("prefill", None, None))
+
+    def call(v, stream):
+        kind, lens, gp = v
+        if kind == "prefill":
+            return kp.prefix_chunk_prefill_attn(qp, c.pool, 0, c.bt[s0:s1], w.prefill_ctx, w.cu_q(), scale=w.scale,
+                                                stream=stream)
+        return kp.paged_decode_attn(q, c.pool, 0, c.bt, lens, group_prefix=gp, scale=w.scale, stream=stream)
+
+    note("many calls in flight: references")
+    refs = [call(v, None) for v in variants]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    note("many calls in flight: 24 calls on two streams")
+    outs = []
+    for k in range(24):
+        s = streams[k % 2]
+        with torch.cuda.stream(s):
+            outs.append((k % len(variants), call(variants[k % len(variants)], s)))
+    torch.cuda.synchronize()
+    for v, out in outs:
+        assert torch.equal(out, refs[v]), f"call of variant {v} differs from the same call made alone"
+
+
 def test_decode_duplicated_prefix_pages_match_shared(cases):
     """Members given private copies of the prompt pages (no sharing) give the shared-page result."""
     w = W.make_workload("rlvr_d64")
