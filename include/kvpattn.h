@@ -72,8 +72,10 @@ typedef enum kvp_dtype { KVP_BF16 = 0, KVP_F32 = 1, KVP_FP8_E4M3 = 2 } kvp_dtype
  *   group_id[i]      host int32 [num_seqs]: group of sequence i, or -1 if ungrouped.
  *   shared_pages[g]  host int32 [num_groups]: the first shared_pages[g] entries of every member's block
  *                    table are the same physical pages (the group's whole prompt pages).
- * For decode it is an optimisation hint: the shared prefix is read once per group and merged with each
- * member's private suffix by a log-sum-exp combine; the result equals the ungrouped result. */
+ * For decode it is an optimisation hint: the shared prefix is read once per group (once per 16 query
+ * columns instead, for wide groups whose prompt is at most about 1% of the call's pages, which keeps the
+ * launch on its fastest form) and merged with each member's private suffix by a log-sum-exp combine;
+ * the result equals the ungrouped result. */
 typedef struct kvp_group_prefix {
   const int32_t* group_id;
   const int32_t* shared_pages;
@@ -153,7 +155,7 @@ int paged_decode_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int nu
  *   q             device bf16 [num_seqs, num_q_heads, head_dim]
  *   block_tables  device int32 [num_seqs, maxp]
  *   seq_lens      host int32 [num_seqs]: cached tokens including the current one (0 = zero output)
- *   group_prefix  host, nullable: members' shared prompt pages are read once per group
+ *   group_prefix  host, nullable: members' shared prompt pages are read once per group (see above)
  *   out           device [num_seqs, num_q_heads, head_dim], out_dtype KVP_BF16 or KVP_F32
  *   ws            device workspace of ws_bytes >= paged_decode_workspace_size(...)
  *   scale         softmax scale applied to q . k (finite, > 0; usually 1 / sqrt(head_dim))
