@@ -202,3 +202,14 @@ def test_binding_refuses_host_tensors():
         kp.kv_append(None, 0, q, q, bt, [0, 0], [0, 1])
     with pytest.raises(ValueError, match="GPU tensor"):
         kp.kv_append(None, 0, q, q, bt, [0, 0], [0, 1, 2])
+
+
+def test_missing_library_fails_loudly():
+    """There is no CPU fallback: without the built library every entry point raises."""
+    code = ("import paper_2608_11152_amd.kvpattn as kp; kp.LIB_PATH = '/nonexistent/libkvpattn.so'\n"
+            "try:\n    kp.kvp_version()\nexcept RuntimeError as e:\n    print('raised', e)\n")
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=root, timeout=120)
+    assert r.returncode == 0 and "raised" in r.stdout and "missing" in r.stdout
