@@ -213,3 +213,15 @@ def test_missing_library_fails_loudly():
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=root, timeout=120)
     assert r.returncode == 0 and "raised" in r.stdout and "missing" in r.stdout
+
+
+def test_product_code_never_imports_the_oracle():
+    """The oracle is test infrastructure: nothing in the package or the C sources imports, links or reads it."""
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    pkg = os.path.join(root, "paper_2608_11152_amd")
+    pat = re.compile(r"^\s*(import\s+oracle|from\s+oracle\b)|#include\s+\"?.*oracle", re.M)
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not pat.search(text), os.path.join(dirpath, f)
