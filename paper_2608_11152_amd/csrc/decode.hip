@@ -611,20 +611,23 @@ __device__ __forceinline__ void decode_wave_block(const DecodeArgs& a, int block
 }
 
 // ---------------------------------------------------------------------------------------------------
-// One launch for both paths: blocks [0, n_wave_blocks) run 4 wave-path waves each; the remaining
-// blocks run the LDS-staged shared-prefix path, one per (prefix item, KV head).  Blocks are dispatched
-// in index order, so the wave blocks take the first round and the shared-prefix blocks run in the
-// slots the planner left free for them.  The two paths need the same number of registers to within a
-// few, so sharing a launch costs no occupancy and saves a launch boundary.
-// ---------------------------------------------------------------------------------------------------
 // Calls without LDS-staged prefix items launch the wave path alone, 8 waves per workgroup: the
 // dispatcher starts workgroups at a bounded rate, so half as many workgroups reach the CUs in about
 // half the time (a 5-6 us ramp instead of 12-13 us for 2048 waves).
+// ---------------------------------------------------------------------------------------------------
 template <int D, bool FP8>
 __global__ __launch_bounds__(512) void decode_wave_kernel(DecodeArgs a) {
   decode_wave_block<D, FP8>(a, blockIdx.x);
 }
 
+// ---------------------------------------------------------------------------------------------------
+// Otherwise one launch covers both paths: blocks [0, n_wave_blocks) run 4 wave-path waves each; the
+// remaining blocks run the LDS-staged shared-prefix path, one per (prefix item, KV head), whose four
+// waves synchronise.  Blocks are dispatched in index order, so the wave blocks take the first round
+// and the shared-prefix blocks run in the slots the planner left free for them.  The two paths need
+// the same number of registers to within a few, so sharing a launch costs no occupancy and saves a
+// launch boundary.
+// ---------------------------------------------------------------------------------------------------
 template <int D, bool FP8>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   constexpr int LB = FP8 ? GroupLds8<D>::bytes : GroupLds<D>::bytes;
@@ -642,11 +645,10 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 // order (so results are deterministic).  Empty partials (m = -inf, l = 0) carry zero weight; a
 // sequence with no partial gets a zero output.  One workgroup per (sequence, KV head, group of hw query
 // heads), started from one 16-byte record {seq, first partial, partial count}; hw is chosen per call so
-// that few sequences still spread over enough workgroups and many do not pay for extra ones.  T = 256 /
-// (hw * D / 4) consecutive lanes
-// share each output float4: lane q loads partials q, q + T, ... (accumulator and (m, l) together, all
-// in flight at once), folds them with a running max, and the T lanes are then combined by shuffles, so
-// the whole merge costs one round of memory latency.
+// that few sequences still spread over enough workgroups and many do not pay for extra ones.
+// T = 256 / (hw * D / 4) consecutive lanes share each output float4: lane q loads partials q, q + T, ...
+// (accumulator and (m, l) together, all in flight at once), folds them with a running max, and the T
+// lanes are then combined by shuffles, so the whole merge costs one round of memory latency.
 // ---------------------------------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
