@@ -89,8 +89,9 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
     if (seq_lens[i] > 0 && shared_of(i) > 0) mem[gp->group_id[i]].push_back(i);
 
   // Units: contiguous page ranges read for one set of query columns.  A group's shared prompt pages
-  // form one unit per subgroup (<= 64 query columns, so the pages are read once per subgroup); each
-  // sequence's pages after its shared prefix form one private unit.
+  // form one unit per subgroup (at most 64 query columns, or 16 when wide groups go to the wave path,
+  // see below), so the pages are read once per subgroup; each sequence's pages after its shared prefix
+  // form one private unit.
   struct Unit {
     int kind, row, lo, hi, tok_end;
     std::vector<int> mems;
