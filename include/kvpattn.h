@@ -6,8 +6,8 @@
  *   - KV state is held in fixed-size blocks of a paged pool, and each session retains a growing set of
  *     blocks (Sec. 2.3 on PagedAttention KV management; Sec. 3.2, the retained blocks k_s(t) of Eq. 2);
  *   - a prompt fans out into grouped samples that share the prompt prefix (Sec. 3.1, group id g_r), and
- *     prefix reuse is block-granular (Sec. 4.4: the longest matching prompt-block hash is the reusable
- *     prefix), so a group shares whole pages;
+ *     prefix reuse is block-granular (Sec. 4.4: a request reuses the leading whole prompt blocks whose
+ *     hashes are cached), so a group shares whole pages;
  *   - a later agentic turn prefills only its L - H new tokens over the cached history H (Eq. 1).
  * The attention itself is scaled dot-product softmax attention with grouped-query heads: query head h
  * reads KV head h / (num_q_heads / num_kv_heads).
@@ -21,7 +21,14 @@
  *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Every call is asynchronous on it.
  *   - Page ids read from device block tables are range-checked on the device.  An id outside
  *     [0, num_pages) is never dereferenced: the kernels skip that page and record KVP_ERANGE in the
- *     pool's device error word, which kv_pool_device_error() returns.
+ *     pool's device error word, which kv_pool_device_error() returns.  Such device-side errors are
+ *     reported after the launch: the call has already returned KVP_OK and the outputs are written (a
+ *     skipped page contributes nothing).  kvp_check_tables() validates a host copy of the tables before
+ *     any launch, for callers that need the error up front.
+ *   - There is no strided-tensor view of a pool layer (its layout below is not a plain strided array):
+ *     kv_pool_layer_ptr() returns the raw layer instead.  Workspace sizes are queried per operation
+ *     (paged_decode_workspace_size, prefix_chunk_prefill_workspace_size) rather than through one query
+ *     taking an operation code.
  *   - Queries are bf16; outputs may be bf16 or fp32.  KV pages are bf16 (KVP_BF16) or OCP FP8 E4M3
  *     (KVP_FP8_E4M3, one byte per element with a per-layer K scale and V scale, see kv_pool_set_scales).
  *   - page_size is 16 tokens; head_dim is 64 or 128; num_q_heads / num_kv_heads is 1, 2, 4, 8 or 16.
@@ -75,7 +82,12 @@ typedef enum kvp_dtype { KVP_BF16 = 0, KVP_F32 = 1, KVP_FP8_E4M3 = 2 } kvp_dtype
  * For decode it is an optimisation hint: the shared prefix is read once per group (once per 16 query
  * columns instead, for wide groups whose prompt is at most about 1% of the call's pages, which keeps the
  * launch on its fastest form) and merged with each member's private suffix by a log-sum-exp combine;
- * the result equals the ungrouped result. */
+ * the result equals the ungrouped result.  The members that read the shared pages together (a group,
+ * or a subgroup of a wide group) read them through the table row of their first decoding member, the
+ * representative.  Because block tables are device-resident, the promise that the other members' first
+ * shared_pages[g] entries equal the representative's is checked on the device: a member whose entries
+ * differ makes the kernels record KVP_EGROUP in the pool's device error word (kv_pool_device_error), and
+ * its output is then attention over the representative's pages for the shared range. */
 typedef struct kvp_group_prefix {
   const int32_t* group_id;
   const int32_t* shared_pages;
@@ -161,7 +173,9 @@ int paged_decode_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int nu
  *   scale         softmax scale applied to q . k (finite, > 0; usually 1 / sqrt(head_dim))
  * Errors: KVP_ERANGE if seq_lens[i] > maxp * 16; KVP_EGROUP if a group id is out of range or a member's
  * seq_len is shorter than its group's shared pages; KVP_EWORKSPACE if ws_bytes is too small; KVP_EINVAL
- * if scale is not finite and positive. */
+ * if scale is not finite and positive.  After the launch (kv_pool_device_error): KVP_ERANGE for a page
+ * id outside the pool, KVP_EGROUP for a member whose shared table entries differ from its group's
+ * representative (see kvp_group_prefix). */
 int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
                       const int32_t* seq_lens, int num_seqs, const kvp_group_prefix* group_prefix,
                       int num_q_heads, float scale, void* out, int out_dtype, void* ws, size_t ws_bytes,
@@ -223,8 +237,8 @@ int kv_restore(kvp_pool_t pool, int layer, const void* host_src, const int32_t* 
                void* stream);
 
 /* ---------------------------------------------------------------------------------------------------
- * Prompt-block hashing and prefix lookup (Sec. 4.4: the engine names every full prompt block by a hash,
- * and the longest matching prompt-block hash is a request's reusable prefix H of Eq. 1)
+ * Prompt-block hashing and prefix lookup (Sec. 4.4: the engine keys every full prompt block by a hash;
+ * a request's reusable prefix H of Eq. 1 is the longest run of its leading blocks whose hashes are cached)
  *
  * Block hash (the paper does not specify one; this is the library's definition, all arithmetic mod 2^64):
  *   mix(z)   = SplitMix64 output function: z += 0x9E3779B97F4A7C15; z = (z ^ z>>30) * 0xBF58476D1CE4E5B9;

@@ -14,7 +14,7 @@ prints no attention formula; it fixes the *structure* of the data this oracle ru
   KV management; Sec. 3.2, the retained blocks k_s(t) of Eq. 2).  A sequence's token at logical position
   t lives in physical page ``block_table[t // 16]`` at slot ``t % 16``.
 * Samples of one rollout group share the prompt prefix (Sec. 3.1, group identity g_r), and reuse is
-  block-granular (Sec. 4.4, longest matching prompt-block hash).  Sharing changes where bytes live, not
+  block-granular (Sec. 4.4: whole prompt blocks are matched by hash).  Sharing changes where bytes live, not
   what attention computes, so this oracle ignores any sharing hint: every sequence is gathered through
   its own block table.
 * A later agentic turn prefills only the uncached L - H tokens over the cached history H (Eq. 1,

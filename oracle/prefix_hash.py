@@ -3,9 +3,9 @@
 Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s ``cpu_baseline`` leg may import this
 module; the product path (the HIP library and its binding) never does and shares no code with it.
 
-Sec. 4.4 of the paper: the inference engine's prefix cache names every full prompt block by a hash, and
-for an incoming request the longest matching prompt-block hash determines the reusable prefix H (the
-H of the prefill cost of Eq. 1).  The paper does not say which hash.  The library's definition, restated
+Sec. 4.4 of the paper: the inference engine's prefix cache keys every full prompt block by a hash; a
+request's reusable prefix H (the H of the prefill cost of Eq. 1) is the longest run of its leading full
+blocks whose hashes the cache holds.  The paper does not say which hash.  The library's definition, restated
 here independently in big-integer Python (all arithmetic mod 2^64):
 
   mix(z)   = the SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014):

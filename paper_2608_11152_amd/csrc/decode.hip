@@ -115,6 +115,14 @@ __device__ __forceinline__ void lane_token_ok(int p, int q4, bool page_ok, int t
   }
 }
 
+// A group hint (kvp_group_prefix) promises that every member's table names the representative row's pages
+// for the shared prefix; the kernels read those pages through the representative row only.  Lanes of the
+// other members compare their own table entry for a page of each step with the row's, and a mismatch is
+// recorded as KVP_EGROUP in the pool's error word (the loads go out with the step's own page-id loads).
+__device__ __forceinline__ void report_group_mismatch(const DecodeArgs& a, bool differs, int lane) {
+  if (__any(differs) && lane == 0) atomicCAS(a.err, 0, KVP_EGROUP);
+}
+
 // Store one column's state: normalised output (slot < 0) or a partial for the merge kernel.
 template <int D, int NT>
 __device__ __forceinline__ void write_state(const DecodeArgs& a, const DecodeItem& it, const SoftState<NT>& st,
@@ -177,13 +185,16 @@ __device__ __forceinline__ void decode_wave_chunk(const DecodeArgs& a, const Dec
   const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
   const uint16_t* hbase = a.layer + (int64_t)kvh * 2 * KB;
   const int32_t* btr = a.bt + (int64_t)it.row * a.maxp;
+  const int32_t* btm = a.bt + (int64_t)seq * a.maxp;
+  const bool chk = it.kind == 1 && col_ok && seq != it.row;  // a member other than the representative
   const int k_off = (c16 & 7) * 8;
   const int v_off = KB + ((q4 & 1) * 16 + c16) * 8;
-  bool bad = false;
+  bool bad = false, differs = false;
   for (int p = it.page_lo; p < it.page_hi; p += 2) {
     const bool has_b = p + 1 < it.page_hi;
     int ida = btr[p];
     int idb = has_b ? btr[p + 1] : ida;
+    if (chk && (!(q4 & 1) || has_b)) differs |= btm[p + (q4 & 1)] != ((q4 & 1) ? idb : ida);
     const bool va = (unsigned)ida < (unsigned)a.num_pages;
     const bool vb = has_b && (unsigned)idb < (unsigned)a.num_pages;
     bad |= !va || (has_b && !vb);
@@ -213,6 +224,7 @@ __device__ __forceinline__ void decode_wave_chunk(const DecodeArgs& a, const Dec
     softmax_pv<NT>(st, sx, sy, a.scale_log2, ok, masked, vv);
   }
   if (bad && lane == 0) atomicCAS(a.err, 0, KVP_ERANGE);
+  report_group_mismatch(a, differs, lane);
   st.l += __shfl_xor(st.l, 16);
   st.l += __shfl_xor(st.l, 32);
   if (col_ok) write_state<D, NT>(a, it, st, seq, head, q4);
@@ -273,7 +285,9 @@ __device__ __forceinline__ void decode_group_block(const DecodeArgs& a, int bloc
   const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
   const uint16_t* hbase = a.layer + (int64_t)kvh * 2 * KB;
   const int32_t* btr = a.bt + (int64_t)it.row * a.maxp;
-  bool bad = false;
+  const int32_t* btm = a.bt + (int64_t)seq * a.maxp;
+  const bool chk = col_ok && seq != it.row;  // a member other than the representative
+  bool bad = false, differs = false;
 
   // Stage pages (p, p+1) into registers; pages past the range or with invalid ids become zeros.
   auto fetch = [&](int p, u32x4 (&r)[NCH]) {
@@ -331,6 +345,7 @@ __device__ __forceinline__ void decode_group_block(const DecodeArgs& a, int bloc
       const bool has_b = p + 1 < it.page_hi;
       const bool va = (unsigned)btr[p] < (unsigned)a.num_pages;
       const bool vb = has_b && (unsigned)btr[p + 1] < (unsigned)a.num_pages;
+      if (chk && (!(q4 & 1) || has_b)) differs |= btm[p + (q4 & 1)] != btr[p + (q4 & 1)];
       const bool masked = !has_b || !va || !vb || (p + 2) * 16 > it.tok_end;
       bool ok[8];
       lane_token_ok(p, q4, q4 < 2 ? va : vb, it.tok_end, ok);
@@ -342,6 +357,7 @@ __device__ __forceinline__ void decode_group_block(const DecodeArgs& a, int bloc
   }
   if (bad && tid == 0) atomicCAS(a.err, 0, KVP_ERANGE);
   if (!wave_on) return;
+  report_group_mismatch(a, differs, lane);
   st.l += __shfl_xor(st.l, 16);
   st.l += __shfl_xor(st.l, 32);
   if (!col_ok) return;
@@ -417,10 +433,13 @@ __device__ __forceinline__ void decode_wave_chunk_fp8(const DecodeArgs& a, const
   const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
   const unsigned char* hbase = reinterpret_cast<const unsigned char*>(a.layer) + (int64_t)kvh * 2 * KB;
   const int32_t* btr = a.bt + (int64_t)it.row * a.maxp;
+  const int32_t* btm = a.bt + (int64_t)seq * a.maxp;
+  const bool chk = it.kind == 1 && col_ok && seq != it.row;  // a member other than the representative
   const int k_off = ((q4)*16 + (c16 & 7)) * 16;                       // + p2 * 1024 (4 chunks of 256 B)
   const int v_off = KB + (((q4 & 1)) * 16 + c16) * 16;                // + y * 512
-  bool bad = false;
+  bool bad = false, differs = false;
   for (int p = it.page_lo; p < it.page_hi; p += 4) {
+    if (chk && p + q4 < it.page_hi) differs |= btm[p + q4] != btr[p + q4];
     int id[4];
     bool val[4], has[4];
 #pragma unroll
@@ -461,6 +480,7 @@ __device__ __forceinline__ void decode_wave_chunk_fp8(const DecodeArgs& a, const
     }
   }
   if (bad && lane == 0) atomicCAS(a.err, 0, KVP_ERANGE);
+  report_group_mismatch(a, differs, lane);
   st.l += __shfl_xor(st.l, 16);
   st.l += __shfl_xor(st.l, 32);
   if (col_ok) write_state<D, NT>(a, it, st, seq, head, q4);
@@ -515,7 +535,9 @@ __device__ __forceinline__ void decode_group_block_fp8(const DecodeArgs& a, int 
   const int64_t page_stride = (int64_t)a.Hkv * 2 * KB;
   const unsigned char* hbase = reinterpret_cast<const unsigned char*>(a.layer) + (int64_t)kvh * 2 * KB;
   const int32_t* btr = a.bt + (int64_t)it.row * a.maxp;
-  bool bad = false;
+  const int32_t* btm = a.bt + (int64_t)seq * a.maxp;
+  const bool chk = col_ok && seq != it.row;  // a member other than the representative
+  bool bad = false, differs = false;
 
   // Stage pages p..p+3 into registers; pages past the range or with invalid ids become zeros.
   auto fetch = [&](int p, u32x4 (&r)[NCH]) {
@@ -553,6 +575,7 @@ __device__ __forceinline__ void decode_group_block_fp8(const DecodeArgs& a, int 
     const bool more = p + 4 < it.page_hi;
     if (more) fetch(p + 4, r);
     if (wave_on) {
+      if (chk && p + q4 < it.page_hi) differs |= btm[p + q4] != btr[p + q4];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int x = p + 2 * u;
@@ -584,6 +607,7 @@ __device__ __forceinline__ void decode_group_block_fp8(const DecodeArgs& a, int 
   }
   if (bad && tid == 0) atomicCAS(a.err, 0, KVP_ERANGE);
   if (!wave_on) return;
+  report_group_mismatch(a, differs, lane);
   st.l += __shfl_xor(st.l, 16);
   st.l += __shfl_xor(st.l, 32);
   if (!col_ok) return;

@@ -4,7 +4,6 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
-#include <cstdlib>
 #include <numeric>
 
 #include "kvp_plan.h"
@@ -43,17 +42,6 @@ Status validate_group_prefix(const int32_t* lens, int B, const kvp_group_prefix*
                   i, lens[i], gp->shared_pages[g]);
   }
   return {};
-}
-
-// Target number of decode waves per call.  KVP_DECODE_WAVES overrides the default for tuning sweeps;
-// the plan stays a pure function of its inputs for a given value.
-static int64_t decode_target_waves() {
-  static const int64_t v = [] {
-    const char* e = std::getenv("KVP_DECODE_WAVES");
-    const long x = e ? std::strtol(e, nullptr, 10) : 0;
-    return x > 0 ? (int64_t)x : (int64_t)2048;
-  }();
-  return v;
 }
 
 Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_prefix* gp, int Hq, int Hkv,
@@ -138,7 +126,7 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   // Wave-path units are cut into equal segments of consecutive pages ("stream-K" over the concatenated
   // unit list): segment s is processed by waves s*Hkv .. s*Hkv+Hkv-1 (one per KV head), so every wave
   // streams the same number of pages whatever the length skew, and a sequence is split only where a
-  // segment boundary falls inside it.  About decode_target_waves() waves: one round of the waves that
+  // segment boundary falls inside it.  About kDecodeWaves waves: one round of the waves that
   // are resident at once on 256 CUs.  Segments hold at least 32 pages (512 tokens) so that a chunk's
   // partial (G x d fp32 written, then read by the merge) stays within ~2% of its KV bytes.
   int64_t total_pages = 0, group_pages = 0;
@@ -148,7 +136,7 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   // Reserve block slots for them out of the one-round budget (4 waves per block), in proportion to
   // their share of the pages weighted by their lower per-block throughput (about 2.5x less than four
   // independent streaming waves), so they drain while the wave segments run instead of after them.
-  const int64_t budget_blocks = std::max<int64_t>(1, decode_target_waves() / 4);
+  const int64_t budget_blocks = std::max<int64_t>(1, kDecodeWaves / 4);
   int64_t reserve = 0;
   if (group_pages > 0) {
     const double wg = 2.5 * (double)group_pages, ww = (double)total_pages;

@@ -1,6 +1,6 @@
-// Block-granular prefix identification (Sec. 4.4 of the paper: the engine's prefix cache names every
-// full prompt block by a hash, and the longest matching prompt-block hash is a request's reusable prefix
-// H).  The paper leaves the hash unspecified; the one defined here is
+// Block-granular prefix identification (Sec. 4.4 of the paper: the engine's prefix cache keys every
+// full prompt block by a hash, and a request's reusable prefix H is the longest run of its leading full
+// blocks whose hashes are cached).  The paper leaves the hash unspecified; the one defined here is
 //
 //   mix(z)    = SplitMix64 output function of z (Steele, Lea and Flood 2014; constants as published):
 //               z += 0x9E3779B97F4A7C15; z = (z ^ z>>30) * 0xBF58476D1CE4E5B9;

@@ -139,6 +139,33 @@ def _stream(stream):
     return C.c_void_p(stream.cuda_stream)
 
 
+def _torch_stream(stream):
+    """The torch stream the library's kernels will run on (the current one when `stream` is None)."""
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream()
+    if isinstance(stream, int):
+        return torch.cuda.ExternalStream(stream)
+    return stream
+
+
+def _alloc_on(stream, shape, dtype, device):
+    """A buffer the kernels enqueued on `stream` write or read: allocated in that stream's context, so the
+    caching allocator does not hand its memory to another stream's allocation while the work is pending."""
+    import torch
+    with torch.cuda.stream(_torch_stream(stream)):
+        return torch.empty(shape, dtype=dtype, device=device)
+
+
+def _check_q_heads(q, pool: "Pool"):
+    """The kernels take head_dim from the pool and the GQA ratio from Hq / num_kv_heads."""
+    _, Hq, d = q.shape
+    if d != pool.head_dim:
+        raise ValueError(f"q has head_dim {d}, the pool {pool.head_dim}")
+    if Hq % pool.num_kv_heads:
+        raise ValueError(f"q has {Hq} heads, not a multiple of the pool's {pool.num_kv_heads} KV heads")
+
+
 def _dptr(t) -> C.c_void_p:
     return C.c_void_p(t.data_ptr() if t is not None else 0)
 
@@ -280,8 +307,8 @@ def kv_gather(pool: Pool, layer, block_tables, lens, stream=None):
     _dev(block_tables, "block_tables", _i32t(), 2, rows=len(ln))
     T = int(ln.sum())
     shape = (T, pool.num_kv_heads, pool.head_dim)
-    k = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
-    v = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    k = _alloc_on(stream, shape, torch.bfloat16, "cuda")
+    v = _alloc_on(stream, shape, torch.bfloat16, "cuda")
     _check(lib().kv_gather(pool.handle, layer, _dptr(block_tables), block_tables.shape[1], _ptr(ln), len(ln),
                            _dptr(k), _dptr(v), _stream(stream)), "kv_gather")
     return k, v
@@ -302,18 +329,19 @@ def paged_decode_attn(q, pool: Pool, layer, block_tables, seq_lens, group_prefix
     sl = _i32(seq_lens)
     _dev(q, "q", _bf16(), 3)
     B, Hq, d = q.shape
+    _check_q_heads(q, pool)
     if B != len(sl):
         raise ValueError(f"q holds {B} sequences, seq_lens {len(sl)}")
     _dev(block_tables, "block_tables", _i32t(), 2, rows=B)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     if out is None:
-        out = torch.empty((B, Hq, d), dtype=out_dtype or torch.float32, device=q.device)
+        out = _alloc_on(stream, (B, Hq, d), out_dtype or torch.float32, q.device)
     _dev(out, "out", _outt(), 3, rows=B, tail=(Hq, d))
     od = KVP_F32 if out.dtype == torch.float32 else KVP_BF16
     gpr = group_prefix if not isinstance(group_prefix, tuple) else _GP(*group_prefix)
     if ws is None:
-        ws = torch.empty(max(1, paged_decode_workspace_size(pool, sl, Hq, gpr)), dtype=torch.uint8, device=q.device)
+        ws = _alloc_on(stream, max(1, paged_decode_workspace_size(pool, sl, Hq, gpr)), torch.uint8, q.device)
     _dev(ws, "ws", (ws.dtype,))
     _check(lib().paged_decode_attn(_dptr(q), pool.handle, layer, _dptr(block_tables), block_tables.shape[1],
                                    _ptr(sl), len(sl), _gp_ref(gpr), Hq, float(scale), _dptr(out), od, _dptr(ws),
@@ -338,18 +366,18 @@ def prefix_chunk_prefill_attn(q, pool: Pool, layer, block_tables, ctx_lens, cu_q
         raise ValueError(f"cu_q has {len(cq)} entries, {len(cl) + 1} needed")
     _dev(q, "q", _bf16(), 3)
     T, Hq, d = q.shape
+    _check_q_heads(q, pool)
     if len(cl) and T != int(cq[-1]):
         raise ValueError(f"q holds {T} rows, cu_q ends at {int(cq[-1])}")
     _dev(block_tables, "block_tables", _i32t(), 2, rows=len(cl))
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     if out is None:
-        out = torch.empty((T, Hq, d), dtype=out_dtype or torch.float32, device=q.device)
+        out = _alloc_on(stream, (T, Hq, d), out_dtype or torch.float32, q.device)
     _dev(out, "out", _outt(), 3, rows=T, tail=(Hq, d))
     od = KVP_F32 if out.dtype == torch.float32 else KVP_BF16
     if ws is None:
-        ws = torch.empty(max(1, prefix_chunk_prefill_workspace_size(pool, cl, cq, Hq)), dtype=torch.uint8,
-                         device=q.device)
+        ws = _alloc_on(stream, max(1, prefix_chunk_prefill_workspace_size(pool, cl, cq, Hq)), torch.uint8, q.device)
     _dev(ws, "ws", (ws.dtype,))
     _check(lib().prefix_chunk_prefill_attn(_dptr(q), pool.handle, layer, _dptr(block_tables), block_tables.shape[1],
                                            _ptr(cl), _ptr(cq), len(cl), Hq, float(scale), _dptr(out), od, _dptr(ws),
@@ -407,7 +435,7 @@ def kvp_block_hashes(tokens, cu_tokens, seed: int = 0, out=None, stream=None):
     if len(cu) and tokens.numel() < int(cu[-1]):
         raise ValueError(f"tokens holds {tokens.numel()} ids, cu_tokens ends at {int(cu[-1])}")
     if out is None:
-        out = torch.empty(max(1, total), dtype=torch.int64, device="cuda")
+        out = _alloc_on(stream, max(1, total), torch.int64, "cuda")
     elif out.numel() < total:
         raise ValueError(f"out holds {out.numel()} hashes, {total} needed")
     _check(lib().kvp_block_hashes(_dptr(tokens), _ptr(cu), len(cu) - 1, C.c_uint64(seed & (2**64 - 1)), _dptr(out),
@@ -419,9 +447,10 @@ def kvp_group_shared_pages(hashes, cu_tokens, group_id, num_groups: int, stream=
     """Shared whole pages of each rollout group, derived on the device; returned on the host."""
     import torch
     cu, gid = _i32(cu_tokens), _i32(group_id)
-    out = torch.empty(max(1, num_groups), dtype=torch.int32, device="cuda")
+    out = _alloc_on(stream, max(1, num_groups), torch.int32, "cuda")
     _check(lib().kvp_group_shared_pages(_dptr(hashes), _ptr(cu), len(cu) - 1, _ptr(gid), num_groups, _dptr(out),
                                         _stream(stream)), "kvp_group_shared_pages")
+    _torch_stream(stream).synchronize()  # the copy below runs on torch's current stream
     return out[:num_groups].cpu().numpy()
 
 
@@ -466,8 +495,8 @@ class PrefixTable:
         total = int(block_hash_offsets(cu)[-1])
         if hashes.numel() < total:
             raise ValueError(f"hashes holds {hashes.numel()} entries, cu_tokens needs {total}")
-        matched = torch.empty(max(1, len(cu) - 1), dtype=torch.int32, device="cuda")
-        pages = torch.empty(max(1, total), dtype=torch.int32, device="cuda")
+        matched = _alloc_on(stream, max(1, len(cu) - 1), torch.int32, "cuda")
+        pages = _alloc_on(stream, max(1, total), torch.int32, "cuda")
         _check(lib().kvp_prefix_lookup(self.handle, _dptr(hashes), _ptr(cu), len(cu) - 1, _dptr(matched),
                                        _dptr(pages), _stream(stream)), "kvp_prefix_lookup")
         return matched[: len(cu) - 1], pages[:total]

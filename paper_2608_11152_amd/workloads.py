@@ -7,8 +7,8 @@ the attention arithmetic, so both the CPU oracle and the GPU path consume exactl
 Workload structure follows the paper's serving model:
   * sessions hold KV in fixed-size blocks of a shared pool (Sec. 3.2, retained blocks k_s(t));
   * a prompt fans out into grouped samples that share the prompt prefix (Sec. 3.1, group id g_r);
-  * prefix reuse is block-granular: the longest matching prompt-block hash defines the reusable prefix
-    (Sec. 4.4), so only whole prompt pages are shared and the partial last prompt page is copied into
+  * prefix reuse is block-granular: a request reuses the leading whole prompt blocks whose hashes are
+    cached (Sec. 4.4), so only whole prompt pages are shared and the partial last prompt page is copied into
     each sample's first private page;
   * a later agentic turn prefills only its new tokens over the cached history (Eq. 1, L_r - H_r);
   * the three classes have the length profiles of Tables 1-2 (RLVR: short prompt, long decode;

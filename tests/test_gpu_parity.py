@@ -175,6 +175,45 @@ def test_many_calls_in_flight_on_two_streams(cases):
         assert torch.equal(out, refs[v]), f"call of variant {v} differs from the same call made alone"
 
 
+def test_default_buffers_belong_to_the_call_stream(cases, monkeypatch):
+    """Calls on a side stream given as an argument (no stream context): the workspace and output the
+    binding allocates must belong to that stream, so memory allocated on the current stream afterwards
+    (while the side stream's kernels may still be pending) never aliases them, and the outputs equal the
+    same calls on the current stream."""
+    import torch
+    c = get_case(cases, "mixed_s")
+    w = c.w
+    q, qp = to_dev_bits(c.vals.q), to_dev_bits(c.vals.qp)
+    s0, s1 = int(w.prefill_seqs[0]), int(w.prefill_seqs[-1]) + 1
+    ref_d = kp.paged_decode_attn(q, c.pool, 0, c.bt, w.decode_len, group_prefix=c.gp, scale=w.scale)
+    ref_p = kp.prefix_chunk_prefill_attn(qp, c.pool, 0, c.bt[s0:s1], w.prefill_ctx, w.cu_q(), scale=w.scale)
+    torch.cuda.synchronize()
+    made = []
+    real = kp._alloc_on
+
+    def spy(stream, shape, dtype, device):
+        t = real(stream, shape, dtype, device)
+        made.append((t.data_ptr(), t.numel() * t.element_size()))
+        return t
+
+    monkeypatch.setattr(kp, "_alloc_on", spy)
+    side = torch.cuda.Stream()
+    note("side-stream calls with binding-allocated buffers")
+    with torch.cuda.stream(side):
+        torch.cuda._sleep(20_000_000)  # keep the side stream busy so its kernels are still pending below
+    out_d = kp.paged_decode_attn(q, c.pool, 0, c.bt, w.decode_len, group_prefix=c.gp, scale=w.scale, stream=side)
+    out_p = kp.prefix_chunk_prefill_attn(qp, c.pool, 0, c.bt[s0:s1], w.prefill_ctx, w.cu_q(), scale=w.scale,
+                                         stream=side)
+    junk = [torch.full((n,), 255, dtype=torch.uint8, device="cuda") for _, n in made]
+    for t in junk:
+        lo, hi = t.data_ptr(), t.data_ptr() + t.numel()
+        assert all(hi <= p0 or p0 + n <= lo for p0, n in made), "current-stream memory aliases a pending buffer"
+    side.synchronize()
+    torch.cuda.synchronize()
+    assert torch.equal(out_d, ref_d) and torch.equal(out_p, ref_p)
+    del junk
+
+
 def test_decode_duplicated_prefix_pages_match_shared(cases):
     """Members given private copies of the prompt pages (no sharing) give the shared-page result."""
     w = W.make_workload("rlvr_d64")
@@ -412,6 +451,12 @@ def test_binding_checks_tensors_before_launch(cases):
         "out of the wrong shape": lambda: kp.paged_decode_attn(q, c.pool, 0, c.bt, lens, out=sentinel[:, :-1]),
         "out in float16": lambda: kp.paged_decode_attn(q, c.pool, 0, c.bt, lens, out=sentinel.half()),
         "host q": lambda: kp.paged_decode_attn(q.cpu(), c.pool, 0, c.bt, lens, out=sentinel),
+        "q with another head_dim than the pool": lambda: kp.paged_decode_attn(
+            torch.zeros((w.B, w.Hq, 2 * w.d), dtype=torch.bfloat16, device="cuda"), c.pool, 0, c.bt, lens,
+            out=sentinel),
+        "q heads not a multiple of the KV heads": lambda: kp.paged_decode_attn(
+            torch.zeros((w.B, w.Hq + 1, w.d), dtype=torch.bfloat16, device="cuda"), c.pool, 0, c.bt, lens,
+            out=sentinel),
     }
     for what, call in bad_calls.items():
         note(f"binding check: {what}")
@@ -432,8 +477,15 @@ def test_binding_checks_tensors_before_launch(cases):
     note("binding check: prefill q rows differ from cu_q")
     with pytest.raises(ValueError):
         kp.prefix_chunk_prefill_attn(qp, c.pool, 0, c.bt, np.array([0], np.int32), cq)
+    sent_p = torch.full((3, w.Hq, w.d), 7.0, device="cuda")
+    for what, qbad in {"another head_dim": torch.zeros((3, w.Hq, 2 * w.d), dtype=torch.bfloat16, device="cuda"),
+                       "heads not a multiple of the KV heads": torch.zeros((3, w.Hq + 1, w.d), dtype=torch.bfloat16,
+                                                                           device="cuda")}.items():
+        note(f"binding check: prefill q with {what}")
+        with pytest.raises(ValueError):
+            kp.prefix_chunk_prefill_attn(qbad, c.pool, 0, c.bt, np.array([0], np.int32), cq, out=sent_p)
     torch.cuda.synchronize()
-    assert torch.all(sentinel == 7.0)
+    assert torch.all(sentinel == 7.0) and torch.all(sent_p == 7.0)
 
 
 def test_bad_page_id_is_skipped_and_reported():
