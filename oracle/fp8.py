@@ -10,7 +10,9 @@ largest finite magnitude is 1.75 * 2^8 = 448.
 Quantisation of a KV element (the library's convention; the paper stores KV in the engine's dtype and
 says nothing about fp8): y = fp32(x) * fp32(1 / scale) in binary32, then y is rounded to the nearest E4M3
 value, ties to the even mantissa; finite |y| beyond 448 saturates to 448; NaN stays NaN.  Dequantisation
-is code value * scale.  Attention over an fp8 pool is the plain attention of the dequantised values.
+is code value * scale.  A scale is a binary32 number (the library's scales are C floats), so a Python
+scale is first rounded to binary32.  Attention over an fp8 pool is the plain attention of the
+dequantised values.
 """
 from __future__ import annotations
 
@@ -57,8 +59,8 @@ def quantize_bf16(bits, scale: float) -> np.ndarray:
 
 
 def dequantize(codes, scale: float) -> np.ndarray:
-    """Exact float64 values code value * scale."""
-    return _VALS[np.asarray(codes, dtype=np.uint8).astype(np.int64)] * float(scale)
+    """Float64 values code value * scale, the scale taken as the binary32 value the library receives."""
+    return _VALS[np.asarray(codes, dtype=np.uint8).astype(np.int64)] * float(np.float32(scale))
 
 
 def dequantize_bf16(codes, scale: float) -> np.ndarray:
