@@ -265,6 +265,51 @@ def fp8_kv_leg(kp, w, vals, gp, bt, step_batches, flush, stream, steps: int, war
     return res
 
 
+def prefill_split_leg(kp, dev, stream, ctx: int = 131072, chunks=(64, 256), reps: int = 10) -> dict:
+    """One agentic session with a long cached history and a short new chunk (Eq. 1's L - H small against
+    H): too few query tiles to fill the GPU, so the planner splits each tile's history into key ranges
+    (partials merged per query row).  GQA 32/4, d = 128, bf16 pages, synthetic N(0, 1) values."""
+    import torch
+    Hq, Hkv, d = 32, 4, 128
+    n = ctx + max(chunks)
+    npg = (n + 15) // 16
+    g = torch.Generator(device=dev)
+    g.manual_seed(1234)
+    perm = torch.randperm(npg + 7, generator=g, device=dev)[:npg].to(torch.int32)[None, :].contiguous()
+    pool = kp.Pool(1, npg + 7, Hkv, d)
+    kv = torch.randn((n, 2, Hkv, d), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    kp.kv_append(pool, 0, kv[:, 0].contiguous(), kv[:, 1].contiguous(), perm, [0], [0, n])
+    del kv
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    res = {"ctx": ctx}
+    for C in chunks:
+        q = torch.randn((C, Hq, d), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+        ws = torch.empty(kp.prefix_chunk_prefill_workspace_size(pool, [ctx], [0, C], Hq), dtype=torch.uint8,
+                         device=dev)
+        out = torch.empty((C, Hq, d), dtype=torch.bfloat16, device=dev)
+        ts = []
+        for it in range(reps + 2):
+            flush.fill_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            kp.prefix_chunk_prefill_attn(q, pool, 0, perm, [ctx], [0, C], out=out, ws=ws)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if it >= 2:
+                ts.append(e0.elapsed_time(e1) / 1e3)
+        t = float(np.median(ts))
+        flops = 4 * d * Hq * (C * ctx + C * (C + 1) // 2)
+        kv_bytes = (ctx + C) * Hkv * d * 2 * 2
+        res[f"C{C}"] = {"ms": round(t * 1e3, 4), "tflops": round(flops / t / 1e12, 2),
+                        "mfma_frac": round(flops / t / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                        "kv_gbs": round(kv_bytes / t / 1e9, 1), "algorithmic_flops": flops, "kv_bytes": kv_bytes}
+    if pool.device_error() != kp.KVP_OK:
+        raise RuntimeError("device error in the split-prefill leg")
+    pool.close()
+    del flush
+    return res
+
+
 def cpu_baseline(w, vals, budget_s: float):
     """Time the CPU fp64 oracle (as it stands) on a bounded sample of the same decode workload."""
     import oracle
@@ -461,6 +506,7 @@ def main():
         res["fp8_kv"]["decode_traffic"] = traffic["decode_fp8"]
         if has_prefill:
             res["fp8_kv"]["prefill_traffic"] = traffic["prefill_fp8"]
+    res["prefill_split"] = prefill_split_leg(kp, dev, stream)
     res["kv_tier"] = kv_tier_leg(kp, pool, w, stream)
     res["prefix_hash"] = prefix_hash_leg(kp, W, w, stream)
     if not args.no_cpu_baseline:

@@ -324,20 +324,29 @@ int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, con
   return KVP_OK;
 }
 
+// Prefill: the caller's workspace holds the metadata (work list, lengths, split bookkeeping, one async
+// copy) followed by the partial states of split tiles [partial accumulators][partial (m, l)].
 struct PrefillLayout {
   kvp::PrefillPlan plan;
   Packer meta;
-  size_t off_items = 0, off_ctx = 0, off_cuq = 0, total = 0;
+  size_t off_items = 0, off_ctx = 0, off_cuq = 0, off_part_base = 0, off_nsplit = 0, off_merge = 0;
+  size_t off_acc = 0, off_ml = 0, total = 0;
 };
 
 int layout_prefill(kvp_pool_t pool, const int32_t* ctx_lens, const int32_t* cu_q, int B, int maxp, int Hq,
                    PrefillLayout* L) {
   kvp::Status st = kvp::plan_prefill(ctx_lens, cu_q, B, maxp, Hq, pool->num_kv_heads, &L->plan);
   if (!st.ok()) return from_status(st);
-  L->off_items = L->meta.add(L->plan.items.data(), L->plan.items.size() * sizeof(kvp::PrefillItem));
+  const auto& P = L->plan;
+  L->off_items = L->meta.add(P.items.data(), P.items.size() * sizeof(kvp::PrefillItem));
   L->off_ctx = L->meta.add(ctx_lens, (size_t)B * 4);
   L->off_cuq = L->meta.add(cu_q, (size_t)(B + 1) * 4);
-  L->total = L->meta.size();
+  L->off_part_base = L->meta.add(P.part_base.data(), P.part_base.size() * 4);
+  L->off_nsplit = L->meta.add(P.nsplit.data(), P.nsplit.size() * 4);
+  L->off_merge = L->meta.add(P.merge_info.data(), P.merge_info.size() * 4);
+  L->off_acc = L->meta.size();
+  L->off_ml = L->off_acc + (((size_t)P.total_parts * Hq * pool->head_dim * 4 + 255) & ~size_t(255));
+  L->total = L->off_ml + (((size_t)P.total_parts * Hq * 8 + 255) & ~size_t(255));
   return KVP_OK;
 }
 
@@ -969,6 +978,10 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
   a.n_items = (int)L.plan.items.size();
   a.ctx_lens = reinterpret_cast<const int32_t*>(w + L.off_ctx);
   a.cu_q = reinterpret_cast<const int32_t*>(w + L.off_cuq);
+  a.part_base = reinterpret_cast<const int32_t*>(w + L.off_part_base);
+  a.nsplit = reinterpret_cast<const int32_t*>(w + L.off_nsplit);
+  a.part_acc = reinterpret_cast<float*>(w + L.off_acc);
+  a.part_ml = reinterpret_cast<float2*>(w + L.off_ml);
   a.out = out;
   a.out_f32 = out_dtype == KVP_F32;
   a.Hq = num_q_heads;
@@ -980,6 +993,19 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
   a.v_scale = a.fp8 ? pool->v_scale[layer] : 1.0f;
   a.err = pool->err;
   hipError_t e = kvp::launch_prefill(a, pool->head_dim, s);
+  if (e == hipSuccess && !L.plan.merge_info.empty()) {
+    // split tiles: combine each query row's key ranges (the decode merge, one record per query row)
+    kvp::MergeArgs mg{};
+    mg.merge_info = reinterpret_cast<const int32_t*>(w + L.off_merge);
+    mg.n_merge = (int)(L.plan.merge_info.size() / 4);
+    mg.part_acc = a.part_acc;
+    mg.part_ml = a.part_ml;
+    mg.out = out;
+    mg.out_f32 = a.out_f32;
+    mg.Hq = num_q_heads;
+    mg.Hkv = pool->num_kv_heads;
+    e = kvp::launch_decode_merge(mg, pool->head_dim, s);
+  }
   return e == hipSuccess ? KVP_OK : hip_err(e, "prefix_chunk_prefill_attn launch");
 }
 

@@ -89,6 +89,10 @@ struct PrefillArgs {
   int n_items;
   const int32_t* ctx_lens;  // device copies
   const int32_t* cu_q;
+  const int32_t* part_base; // [B] first partial of each session (split sessions only)
+  const int32_t* nsplit;    // [B] key ranges per query row
+  float* part_acc;          // [parts, Hq, D] unnormalised accumulators of split tiles
+  float2* part_ml;          // [parts, Hq] (running max in log2 units, weight sum)
   void* out;
   int out_f32;
   int Hq, Hkv, G, num_pages;

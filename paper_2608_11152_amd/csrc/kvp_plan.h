@@ -45,18 +45,28 @@ struct DecodePlan {
   int32_t group_reserved_blocks = 0;    // block slots the wave budget leaves to the shared-prefix path
 };
 
-// Prefill: one 4-wave workgroup per (session, kv head, 128-row query tile).
+// Prefill: one 4-wave workgroup per (session, kv head, 128-row query tile, key range).  The key range is
+// a run of 64-key stages [st_lo, st_hi) (st_hi is clamped to the tile's own last stage); a tile whose
+// history is split over several workgroups writes one partial softmax state per range, merged per query
+// row by log-sum-exp afterwards.
 struct PrefillItem {
   int32_t seq;       // session index (block-table row)
   int32_t kvh;       // KV head
   int32_t row0;      // first flattened query row (position * G + head-in-group) of the tile
-  int32_t pad;
+  int32_t st_lo;     // first 64-key stage of the range (st_lo * 64 <= the session's cached length)
+  int32_t st_hi;     // one past the last stage of the range
+  int32_t slot;      // partial index of the range within each query row's list, -1 = write the output
+  int32_t pad[2];
 };
-static_assert(sizeof(PrefillItem) == 16, "PrefillItem is uploaded as raw bytes");
+static_assert(sizeof(PrefillItem) == 32, "PrefillItem is uploaded as raw bytes");
 
 struct PrefillPlan {
   std::vector<PrefillItem> items;  // blockIdx order (XCD-aware, empty entries have seq = -1)
   int64_t real_items = 0;
+  std::vector<int32_t> nsplit;     // [B] key ranges per query row of each session (1 = not split)
+  std::vector<int32_t> part_base;  // [B] first partial of each session (its row r owns part_base + r * nsplit)
+  std::vector<int32_t> merge_info; // per merged query row: {row in q / out, first partial, nsplit, 0}
+  int32_t total_parts = 0;
 };
 
 struct Status {
@@ -74,5 +84,9 @@ Status check_tables(const int32_t* bt, int maxp, const int32_t* lens, int B, int
                     const kvp_group_prefix* gp);
 
 constexpr int kPrefillRows = 128;  // flattened query rows per prefill workgroup
+// A call whose tiles (x their 64-key stages) would not give about this many equal workgroups splits
+// tile histories into key ranges: two resident 64 KB-LDS workgroups per CU on 256 CUs.
+constexpr int kPrefillSplitTarget = 512;
+constexpr int kPrefillMinSplitStages = 16;  // smallest key range of a split (1024 keys)
 
 }  // namespace kvp

@@ -248,24 +248,88 @@ Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int max
       return fail(KVP_ERANGE, "ctx_lens[%ld] + chunk = %ld exceeds maxp * 16 = %ld", i,
                   (long)ctx_lens[i] + C, (long)maxp * kPage);
   }
-  // Units = contiguous runs of query tiles of one (session, kv head).  Tiles of a unit read the same
-  // KV, so a unit is kept on one XCD (workgroup b runs on XCD b % 8) to share that XCD's L2.  Units are
-  // spread over the 8 XCDs longest-first; within an XCD the heaviest units start first.
-  struct Unit { int seq, kvh, t0, t1; double w; };
+  // History split.  Long histories under few query tiles (a short uncached suffix over a long cached
+  // prefix, Eq. 1) would leave most CUs idle: each tile streams its whole history alone.  When the
+  // call's tiles are fewer than kPrefillSplitTarget, each tile's 64-key stages are cut into ranges of
+  // about T stages, T chosen so that the call holds about kPrefillSplitTarget ranges (at least
+  // kPrefillMinSplitStages stages each).  A range may start only at a stage whose first key every query
+  // row of the session sees (st * 64 <= ctx), so every range is non-empty for every row; the ranges of
+  // one session are shared by all its tiles and the last one runs to each tile's own last stage.
+  auto tile_stages = [&](int i, int t) {
+    const int64_t C = cu_q[i + 1] - cu_q[i];
+    const int64_t last_row = std::min<int64_t>(C * G - 1, (int64_t)t * kPrefillRows + kPrefillRows - 1);
+    return (int)((ctx_lens[i] + last_row / G + 1 + 63) / 64);
+  };
+  plan->nsplit.assign(B, 1);
+  plan->part_base.assign(B, 0);
+  std::vector<std::vector<int>> bounds(B);  // split starts after 0, per session
+  {
+    int64_t tiles_total = 0, work = 0;
+    for (int i = 0; i < B; ++i) {
+      const int C = cu_q[i + 1] - cu_q[i];
+      const int nt = (int)(((int64_t)C * G + kPrefillRows - 1) / kPrefillRows);
+      tiles_total += (int64_t)nt * Hkv;
+      for (int t = 0; t < nt; ++t) work += (int64_t)tile_stages(i, t) * Hkv;
+    }
+    if (tiles_total > 0 && tiles_total < kPrefillSplitTarget) {
+      const int64_t T = std::max<int64_t>(kPrefillMinSplitStages, (work + kPrefillSplitTarget - 1) / kPrefillSplitTarget);
+      for (int i = 0; i < B; ++i) {
+        const int C = cu_q[i + 1] - cu_q[i];
+        if (C == 0) continue;
+        const int nst = tile_stages(i, 0);             // the session's shortest tile
+        const int max_start = ctx_lens[i] / 64;        // latest stage a range may start at
+        const int64_t want = (nst + T - 1) / T;
+        const int S = (int)std::min<int64_t>(want, (int64_t)max_start + 1);
+        for (int k = 1; k < S; ++k) {
+          const int b = std::min<int>(max_start, (int)((int64_t)k * nst / S));
+          if (b > (bounds[i].empty() ? 0 : bounds[i].back())) bounds[i].push_back(b);
+        }
+        plan->nsplit[i] = (int)bounds[i].size() + 1;
+      }
+    }
+  }
+  int32_t parts = 0;
+  for (int i = 0; i < B; ++i) {
+    if (plan->nsplit[i] == 1) continue;
+    const int C = cu_q[i + 1] - cu_q[i];
+    plan->part_base[i] = parts;
+    for (int j = 0; j < C; ++j) {
+      const int32_t rec[4] = {cu_q[i] + j, parts + j * plan->nsplit[i], plan->nsplit[i], 0};
+      plan->merge_info.insert(plan->merge_info.end(), rec, rec + 4);
+    }
+    if ((int64_t)parts + (int64_t)C * plan->nsplit[i] > INT32_MAX) return fail(KVP_EINVAL, "too many partials");
+    parts += C * plan->nsplit[i];
+  }
+  plan->total_parts = parts;
+
+  // Units = contiguous runs of query tiles of one (session, kv head, key range).  Tiles of a unit read
+  // the same KV, so a unit is kept on one XCD (workgroup b runs on XCD b % 8) to share that XCD's L2.
+  // Units are spread over the 8 XCDs longest-first; within an XCD the heaviest units start first.
+  struct Unit { int seq, kvh, t0, t1, k; double w; };
   std::vector<Unit> units;
   int64_t tiles_total = 0;
-  for (int i = 0; i < B; ++i) tiles_total += (int64_t)((cu_q[i + 1] - cu_q[i]) * G + kPrefillRows - 1) / kPrefillRows * Hkv;
+  for (int i = 0; i < B; ++i)
+    tiles_total += ((int64_t)(cu_q[i + 1] - cu_q[i]) * G + kPrefillRows - 1) / kPrefillRows * Hkv * plan->nsplit[i];
   const int64_t seg = std::max<int64_t>(1, tiles_total / 64);  // at least ~64 units to balance 8 XCDs
+  auto range_of = [&](int i, int k, int t, int* lo, int* hi) {
+    *lo = k == 0 ? 0 : bounds[i][k - 1];
+    *hi = k + 1 < plan->nsplit[i] ? bounds[i][k] : tile_stages(i, t);
+  };
   for (int i = 0; i < B; ++i) {
     const int C = cu_q[i + 1] - cu_q[i];
-    const int nt = (C * G + kPrefillRows - 1) / kPrefillRows;
+    const int nt = (int)(((int64_t)C * G + kPrefillRows - 1) / kPrefillRows);
     for (int h = 0; h < Hkv; ++h)
-      for (int t0 = 0; t0 < nt; t0 += (int)seg) {
-        const int t1 = std::min<int>(nt, t0 + (int)seg);
-        double w = 0;
-        for (int t = t0; t < t1; ++t) w += ctx_lens[i] + std::min(C - 1, (t * kPrefillRows + kPrefillRows - 1) / G) + 1;
-        units.push_back(Unit{i, h, t0, t1, w});
-      }
+      for (int k = 0; k < plan->nsplit[i]; ++k)
+        for (int t0 = 0; t0 < nt; t0 += (int)seg) {
+          const int t1 = std::min<int>(nt, t0 + (int)seg);
+          double w = 0;
+          for (int t = t0; t < t1; ++t) {
+            int lo, hi;
+            range_of(i, k, t, &lo, &hi);
+            w += hi - lo;
+          }
+          units.push_back(Unit{i, h, t0, t1, k, w});
+        }
   }
   std::vector<int> order(units.size());
   std::iota(order.begin(), order.end(), 0);
@@ -276,12 +340,17 @@ Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int max
   for (int u : order) {
     const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
     load[x] += units[u].w;
-    for (int t = units[u].t0; t < units[u].t1; ++t)
-      bins[x].push_back(PrefillItem{units[u].seq, units[u].kvh, t * kPrefillRows, 0});
+    const Unit& un = units[u];
+    for (int t = un.t0; t < un.t1; ++t) {
+      int lo, hi;
+      range_of(un.seq, un.k, t, &lo, &hi);
+      bins[x].push_back(PrefillItem{un.seq, un.kvh, t * kPrefillRows, lo, hi,
+                                    plan->nsplit[un.seq] == 1 ? -1 : un.k, {0, 0}});
+    }
   }
   size_t longest = 0;
   for (auto& b : bins) longest = std::max(longest, b.size());
-  plan->items.assign(longest * kXcd, PrefillItem{-1, 0, 0, 0});
+  plan->items.assign(longest * kXcd, PrefillItem{-1, 0, 0, 0, 0, -1, {0, 0}});
   for (int x = 0; x < kXcd; ++x)
     for (size_t j = 0; j < bins[x].size(); ++j) plan->items[j * kXcd + x] = bins[x][j];
   plan->real_items = tiles_total;

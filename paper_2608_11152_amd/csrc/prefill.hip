@@ -1,7 +1,7 @@
 // Chunked prefill of a new turn over a cached history (Eq. 1 of the paper: a later agentic turn only
 // prefills its L - H uncached tokens; they attend to the cached H tokens and causally to each other).
 //
-// One 4-wave workgroup per (session, KV head, 128 flattened query rows).  Query rows are flattened as
+// One 4-wave workgroup per (session, KV head, 128 flattened query rows, key range).  Query rows are flattened as
 // position * G + head-in-group, so every K/V tile loaded serves all G query heads of its KV head.  Keys
 // stream through LDS in stages of 4 pages (64 keys), double-buffered: the next stage is loaded into
 // registers while this stage's MFMA work runs, then stored to the other buffer.  Wave w owns 32 query
@@ -9,6 +9,9 @@
 //   S^T (64 keys x 32 rows) = K Q^T      v_mfma_f32_32x32x16_bf16, 2 key tiles x D/16 k-steps
 //   O^T (D x 32 rows)      += V^T P^T    the score tile's registers are the P^T operand (per page)
 // Masking is applied only to stages that reach past the wave's first query position (the diagonal).
+// A tile whose history the planner split into key ranges (few tiles over long histories) writes, per
+// range, the unnormalised partial state (running max, weight sum, accumulator) instead of its output;
+// the decode path's log-sum-exp merge kernel then combines the ranges of each query row.
 #include "kvp_kernels.h"
 #include "kvp_layout.h"
 
@@ -78,7 +81,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   const int n_keys = ctx + (min(nrows - 1, it.row0 + 127) / G) + 1;  // keys any row of the tile sees
   const int wave_min_pos = ctx + min(it.row0 + wv * 32, nrows - 1) / G;
   const int n_pages = (n_keys + 15) / 16;
-  const int n_stages = (n_keys + 63) / 64;
+  const int st_end = min(it.st_hi, (n_keys + 63) / 64);  // this workgroup's key range: stages [st_lo, st_end)
 
   u32x4 qt[NS];
   {
@@ -216,16 +219,16 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     }
   };
   unsigned okm;  // bit pg: page pg of the stage in flight is valid
-  fetch(0, okm);
-  store_stage(0, 0, okm);
+  fetch(it.st_lo, okm);
+  store_stage(it.st_lo, 0, okm);
   // All earlier global loads (the query fragments) have landed: without this, the compiler's waits
   // for them inside the loop would also wait for each step's staging loads.
   __builtin_amdgcn_s_waitcnt(0x0F70);
-  patch(0, 0, okm);
+  patch(it.st_lo, 0, okm);
   __syncthreads();
   int buf = 0;
-  for (int st = 0; st < n_stages; ++st) {
-    const bool more = st + 1 < n_stages;
+  for (int st = it.st_lo; st < st_end; ++st) {
+    const bool more = st + 1 < st_end;
     if (more) fetch(st + 1, okm);
     const unsigned char* sb = lds + buf * SB;
     // The two 32-key tiles' MFMA chains are interleaved.  K operands are read from LDS KD k-steps ahead
@@ -264,7 +267,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     __builtin_amdgcn_sched_barrier(0);
     // Softmax against a reference max.  With c = scale * log2(e) > 0 (the host rejects other scales),
     // the weights are exp2(c*s - m_run), m_run being the running row max of the earlier stages (exact
-    // from stage 0 on, since every row sees key 0 there).  The stage's own max is taken only at stage 0
+    // from the range's first stage on: every row sees that stage's first key, which the planner
+    // guarantees).  The stage's own max is taken only at that first stage
     // or when a lane's weight sum passes 256 (some score rose above m_run): otherwise every weight is at
     // most 256 and, numerator and denominator sharing the reference, the result is unchanged.  So the
     // common path has no max reduction: one FMA and one exponential per score.
@@ -299,7 +303,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         for (int w = 0; w < 4; ++w) pb[pg][w] = pack_bf16(p[2 * w], p[2 * w + 1]);
       }
     };
-    bool slow = st == 0;
+    bool slow = st == it.st_lo;
     if (!slow) {
       weights(m_run);
       slow = __any(!(ssum <= 256.0f));
@@ -311,7 +315,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
       mx = fmaxf(mx, t[31]);
       mx = fmaxf(mx, __shfl_xor(mx, 32)) * cs;
       const float mnew = fmaxf(m_run, mx);
-      const float alpha = fast_exp2(m_run - mnew);  // 0 at stage 0 (m_run = -inf), where acc and l are 0
+      const float alpha = fast_exp2(m_run - mnew);  // 0 at the first stage (m_run = -inf), acc and l are 0
       m_run = mnew;
       l_run *= alpha;
 #pragma unroll
@@ -338,6 +342,21 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
   if (bad) atomicCAS(a.err, 0, KVP_ERANGE);
   l_run += __shfl_xor(l_run, 32);
   if (!row_ok) return;
+  if (it.slot >= 0) {
+    // One key range of a split tile: the partial state of this query row, for the merge.
+    const int64_t pidx = (int64_t)a.part_base[it.seq] + (int64_t)fpos * a.nsplit[it.seq] + it.slot;
+    const int head = it.kvh * G + hl;
+    float* pa = a.part_acc + (pidx * a.Hq + head) * D + 4 * g;
+#pragma unroll
+    for (int d = 0; d < NDT; ++d)
+#pragma unroll
+      for (int t4 = 0; t4 < 4; ++t4)
+        *reinterpret_cast<float4*>(pa + 32 * d + 8 * t4) =
+            make_float4(acc[d][4 * t4] * a.v_scale, acc[d][4 * t4 + 1] * a.v_scale, acc[d][4 * t4 + 2] * a.v_scale,
+                        acc[d][4 * t4 + 3] * a.v_scale);
+    if (g == 0) a.part_ml[pidx * a.Hq + head] = make_float2(m_run, l_run);
+    return;
+  }
   const float inv = l_run > 0.0f ? a.v_scale / l_run : 0.0f;
   const int64_t o = ((int64_t)(q0 + fpos) * a.Hq + it.kvh * G + hl) * D + 4 * g;
 #pragma unroll
