@@ -323,6 +323,11 @@ __device__ __forceinline__ void decode_group_block(const DecodeArgs& a, int bloc
   int buf = 0;
   for (int p = it.page_lo; p < it.page_hi; p += 2) {
     const bool more = p + 2 < it.page_hi;
+    // Group-hint check of this step's pages, loaded before the next step's staging loads so that the
+    // comparison below waits only for these two loads, not for the staging ones.
+    const int pc = min(p + (q4 & 1), it.page_hi - 1);
+    const int mine = btm[pc], theirs = btr[pc];
+    __builtin_amdgcn_sched_barrier(0);
     if (more) fetch(p + 2, r);
     if (wave_on) {
       const unsigned char* sb = lds + buf * SB;
@@ -345,12 +350,12 @@ __device__ __forceinline__ void decode_group_block(const DecodeArgs& a, int bloc
       const bool has_b = p + 1 < it.page_hi;
       const bool va = (unsigned)btr[p] < (unsigned)a.num_pages;
       const bool vb = has_b && (unsigned)btr[p + 1] < (unsigned)a.num_pages;
-      if (chk && (!(q4 & 1) || has_b)) differs |= btm[p + (q4 & 1)] != btr[p + (q4 & 1)];
       const bool masked = !has_b || !va || !vb || (p + 2) * 16 > it.tok_end;
       bool ok[8];
       lane_token_ok(p, q4, q4 < 2 ? va : vb, it.tok_end, ok);
       softmax_pv<NT>(st, sx, sy, a.scale_log2, ok, masked, vv);
     }
+    differs |= chk && mine != theirs;
     if (more) store(buf ^ 1, r);
     __syncthreads();
     buf ^= 1;
@@ -439,13 +444,19 @@ __device__ __forceinline__ void decode_wave_chunk_fp8(const DecodeArgs& a, const
   const int v_off = KB + (((q4 & 1)) * 16 + c16) * 16;                // + y * 512
   bool bad = false, differs = false;
   for (int p = it.page_lo; p < it.page_hi; p += 4) {
-    if (chk && p + q4 < it.page_hi) differs |= btm[p + q4] != btr[p + q4];
     int id[4];
     bool val[4], has[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       has[j] = p + j < it.page_hi;
       id[j] = has[j] ? btr[p + j] : 0;
+    }
+    // group-hint check: the member's entry for page p + q4 is loaded with the step's page ids
+    const bool ck = chk && p + q4 < it.page_hi;
+    const int mine = ck ? btm[p + q4] : 0;
+    differs |= ck && mine != (q4 == 0 ? id[0] : q4 == 1 ? id[1] : q4 == 2 ? id[2] : id[3]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
       val[j] = has[j] && (unsigned)id[j] < (unsigned)a.num_pages;
       bad |= has[j] && !val[j];
       if (!val[j]) id[j] = 0;
@@ -573,9 +584,13 @@ __device__ __forceinline__ void decode_group_block_fp8(const DecodeArgs& a, int 
   int buf = 0;
   for (int p = it.page_lo; p < it.page_hi; p += 4) {
     const bool more = p + 4 < it.page_hi;
+    // Group-hint check of this step's pages, loaded before the next step's staging loads (see the bf16
+    // block).
+    const int pc = min(p + q4, it.page_hi - 1);
+    const int mine = btm[pc], theirs = btr[pc];
+    __builtin_amdgcn_sched_barrier(0);
     if (more) fetch(p + 4, r);
     if (wave_on) {
-      if (chk && p + q4 < it.page_hi) differs |= btm[p + q4] != btr[p + q4];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int x = p + 2 * u;
@@ -601,6 +616,7 @@ __device__ __forceinline__ void decode_group_block_fp8(const DecodeArgs& a, int 
         fp8_substep<NS, NT>(st, qt, kxr, kyr, vr, a.scale_log2, ok, masked);
       }
     }
+    differs |= chk && mine != theirs;
     if (more) store(buf ^ 1, r);
     __syncthreads();
     buf ^= 1;
