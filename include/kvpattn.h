@@ -181,6 +181,23 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
                       int num_q_heads, float scale, void* out, int out_dtype, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* paged_decode_attn without any allocation, for callers that cannot allocate memory during the call
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  Same arguments,
+ * results and errors as paged_decode_attn, bitwise-identical outputs, but no workspace argument: the work
+ * list and the split-KV partial states live in a scratch array of KVP_NOALLOC_SCRATCH_BYTES that the
+ * library's code object holds in device memory (one copy per GPU, kept until the process ends), and the
+ * work list reaches it through kernel launch arguments, so the call allocates neither device nor pinned
+ * host memory.  The pool must live on the current device (else KVP_EINVAL).  A call whose work list plus
+ * partials exceed the scratch returns KVP_EWORKSPACE before anything is enqueued (the RLVR batch of 512
+ * sequences over 1k-16k tokens needs about 37 MiB).  Every call on one GPU shares that GPU's scratch, and
+ * nothing in it needs clearing between calls: calls on one stream are ordered, but calls that overlap on
+ * one GPU (concurrent streams, or host threads) race on the scratch and must be serialised by the
+ * caller. */
+#define KVP_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int paged_decode_attn_noalloc(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
+                              const int32_t* seq_lens, int num_seqs, const kvp_group_prefix* group_prefix,
+                              int num_q_heads, float scale, void* out, int out_dtype, void* stream);
+
 /* ---------------------------------------------------------------------------------------------------
  * prefix_chunk_prefill_attn — a new chunk attends to its cached history plus itself (Eq. 1: only the
  * L - H uncached tokens are prefilled over the reusable prefix H)

@@ -32,6 +32,13 @@ struct kvp_pool {
   int* err = nullptr;             // device error word
 };
 
+// Scratch of the allocation-free decode entry point: the work list and the split-KV partials of one
+// call, in device memory the code object brings (every GPU the library runs on holds its own copy until
+// the process ends).  Host code never passes the array's name to a kernel: it uses the device address
+// hipGetSymbolAddress returns for the current device (scratch_of).
+constexpr size_t kNoAllocScratchBytes = KVP_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -144,6 +151,25 @@ class Staging {
 Staging& staging() {
   static Staging* s = new Staging();  // intentionally leaked: outlives static destruction order
   return *s;
+}
+
+// Device address of `scratch` on device `dev` (the current device), looked up once per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned char* g_scratch_addr[kMaxDevices] = {};
+
+int scratch_of(int dev, unsigned char** out) {
+  if (dev < 0 || dev >= kMaxDevices) return set_err(KVP_EINVAL, "device %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_err(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return set_err(KVP_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_addr[dev] = reinterpret_cast<unsigned char*>(p);
+  }
+  *out = g_scratch_addr[dev];
+  return KVP_OK;
 }
 
 // Packs several arrays into one host buffer with 256-byte aligned offsets.
@@ -326,6 +352,67 @@ int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, con
 
 // Prefill: the caller's workspace holds the metadata (work list, lengths, split bookkeeping, one async
 // copy) followed by the partial states of split tiles [partial accumulators][partial (m, l)].
+// Launches the decode kernels (and the merge) for a laid-out plan whose metadata sits at `meta` (pinned
+// host memory or device memory) and whose partial states go to `part` (device memory of L.total bytes).
+hipError_t launch_decode_plan(const DecodeLayout& L, kvp_pool_t pool, int layer, const void* q,
+                              const int32_t* block_tables, int maxp, int num_q_heads, float scale, void* out,
+                              int out_dtype, const unsigned char* meta, unsigned char* part, hipStream_t s) {
+  const auto& P = L.plan;
+  kvp::DecodeArgs a{};
+  a.q = reinterpret_cast<const uint16_t*>(q);
+  a.layer = layer_ptr(pool, layer);
+  a.bt = block_tables;
+  a.maxp = maxp;
+  a.members = reinterpret_cast<const int32_t*>(meta + L.off_members);
+  a.part_base = reinterpret_cast<const int32_t*>(meta + L.off_part_base);
+  a.part_acc = reinterpret_cast<float*>(part + L.off_acc);
+  a.part_ml = reinterpret_cast<float2*>(part + L.off_ml);
+  a.out = out;
+  a.out_f32 = out_dtype == KVP_F32;
+  a.Hq = num_q_heads;
+  a.Hkv = pool->num_kv_heads;
+  a.G = num_q_heads / pool->num_kv_heads;
+  a.num_pages = pool->num_pages;
+  a.fp8 = pool->dtype == KVP_FP8_E4M3;
+  a.scale_log2 = scale * 1.4426950408889634f * (a.fp8 ? pool->k_scale[layer] : 1.0f);
+  a.v_scale = a.fp8 ? pool->v_scale[layer] : 1.0f;
+  a.err = pool->err;
+  a.items = reinterpret_cast<const kvp::DecodeItem*>(meta + L.off_wave);
+  a.seg_off = reinterpret_cast<const int32_t*>(meta + L.off_seg);
+  a.n_items = (int)P.seg_off.size() - 1;
+  a.group_items = reinterpret_cast<const kvp::DecodeItem*>(meta + L.off_group);
+  a.n_group_items = (int)P.group_items.size();
+  a.n_group_blocks = a.n_group_items * a.Hkv;
+  a.n_wave_blocks = (a.n_items * a.Hkv + 3) / 4;
+  hipError_t e = kvp::launch_decode(a, pool->head_dim, s);
+  if (e == hipSuccess && !P.merge_seqs.empty()) {
+    kvp::MergeArgs mg{};
+    mg.merge_info = reinterpret_cast<const int32_t*>(meta + L.off_merge);
+    mg.n_merge = (int)P.merge_seqs.size();
+    mg.part_acc = a.part_acc;
+    mg.part_ml = a.part_ml;
+    mg.out = out;
+    mg.out_f32 = a.out_f32;
+    mg.Hq = num_q_heads;
+    mg.Hkv = pool->num_kv_heads;
+    e = kvp::launch_decode_merge(mg, pool->head_dim, s);
+  }
+  return e;
+}
+
+// Checks shared by the decode entry points (before anything is planned or enqueued).
+int check_decode_args(kvp_pool_t pool, int layer, const void* q, const int32_t* block_tables,
+                      const int32_t* seq_lens, int num_seqs, float scale, const void* out, int out_dtype) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
+  if (num_seqs == 0) return KVP_OK;
+  if (!q || !out || !block_tables || !seq_lens) return set_err(KVP_EINVAL, "NULL pointer argument");
+  if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
+  if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
+  return KVP_OK;
+}
+
 struct PrefillLayout {
   kvp::PrefillPlan plan;
   Packer meta;
@@ -872,20 +959,14 @@ int paged_decode_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int nu
 int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
                       const int32_t* seq_lens, int num_seqs, const kvp_group_prefix* group_prefix, int num_q_heads,
                       float scale, void* out, int out_dtype, void* ws, size_t ws_bytes, void* stream) {
-  int rc = check_layer(pool, layer);
-  if (rc) return rc;
-  if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
-  if (num_seqs == 0) return KVP_OK;
-  if (!q || !out || !block_tables || !seq_lens) return set_err(KVP_EINVAL, "NULL pointer argument");
-  if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
-  if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
+  int rc = check_decode_args(pool, layer, q, block_tables, seq_lens, num_seqs, scale, out, out_dtype);
+  if (rc || num_seqs == 0) return rc;
   DecodeLayout L;
   rc = layout_decode(pool, seq_lens, num_seqs, maxp, group_prefix, num_q_heads, &L);
   if (rc) return rc;
   if (L.total > 0 && (!ws || ws_bytes < L.total))
     return set_err(KVP_EWORKSPACE, "workspace of %zu bytes, %zu needed", ws ? ws_bytes : (size_t)0, L.total);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  unsigned char* w = reinterpret_cast<unsigned char*>(ws);
   // The work list is read by the kernels straight from a pinned staging slot (a few KB to a few
   // hundred KB, read once per wave), so no copy sits between the caller's previous work and the
   // decode kernels.  The slot is released after the last kernel that reads it.
@@ -893,50 +974,42 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   rc = staging().lease(L.meta.buf.size(), &lease);
   if (rc) return rc;
   std::memcpy(lease.host, L.meta.buf.data(), L.meta.buf.size());
-  const unsigned char* m = reinterpret_cast<const unsigned char*>(lease.host);
-  const auto& P = L.plan;
-  kvp::DecodeArgs a{};
-  a.q = reinterpret_cast<const uint16_t*>(q);
-  a.layer = layer_ptr(pool, layer);
-  a.bt = block_tables;
-  a.maxp = maxp;
-  a.members = reinterpret_cast<const int32_t*>(m + L.off_members);
-  a.part_base = reinterpret_cast<const int32_t*>(m + L.off_part_base);
-  a.part_acc = reinterpret_cast<float*>(w + L.off_acc);
-  a.part_ml = reinterpret_cast<float2*>(w + L.off_ml);
-  a.out = out;
-  a.out_f32 = out_dtype == KVP_F32;
-  a.Hq = num_q_heads;
-  a.Hkv = pool->num_kv_heads;
-  a.G = num_q_heads / pool->num_kv_heads;
-  a.num_pages = pool->num_pages;
-  a.fp8 = pool->dtype == KVP_FP8_E4M3;
-  a.scale_log2 = scale * 1.4426950408889634f * (a.fp8 ? pool->k_scale[layer] : 1.0f);
-  a.v_scale = a.fp8 ? pool->v_scale[layer] : 1.0f;
-  a.err = pool->err;
-  a.items = reinterpret_cast<const kvp::DecodeItem*>(m + L.off_wave);
-  a.seg_off = reinterpret_cast<const int32_t*>(m + L.off_seg);
-  a.n_items = (int)P.seg_off.size() - 1;
-  a.group_items = reinterpret_cast<const kvp::DecodeItem*>(m + L.off_group);
-  a.n_group_items = (int)P.group_items.size();
-  a.n_group_blocks = a.n_group_items * a.Hkv;
-  a.n_wave_blocks = (a.n_items * a.Hkv + 3) / 4;
-  hipError_t e = kvp::launch_decode(a, pool->head_dim, s);
-  if (e == hipSuccess && !P.merge_seqs.empty()) {
-    kvp::MergeArgs mg{};
-    mg.merge_info = reinterpret_cast<const int32_t*>(m + L.off_merge);
-    mg.n_merge = (int)P.merge_seqs.size();
-    mg.part_acc = a.part_acc;
-    mg.part_ml = a.part_ml;
-    mg.out = out;
-    mg.out_f32 = a.out_f32;
-    mg.Hq = num_q_heads;
-    mg.Hkv = pool->num_kv_heads;
-    e = kvp::launch_decode_merge(mg, pool->head_dim, s);
-  }
+  hipError_t e = launch_decode_plan(L, pool, layer, q, block_tables, maxp, num_q_heads, scale, out, out_dtype,
+                                    reinterpret_cast<const unsigned char*>(lease.host),
+                                    reinterpret_cast<unsigned char*>(ws), s);
   const int rr = staging().release(lease, s, e == hipSuccess);
   if (e != hipSuccess) return hip_err(e, "paged_decode_attn launch");
   return rr;
+}
+
+int paged_decode_attn_noalloc(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
+                              const int32_t* seq_lens, int num_seqs, const kvp_group_prefix* group_prefix,
+                              int num_q_heads, float scale, void* out, int out_dtype, void* stream) {
+  int rc = check_decode_args(pool, layer, q, block_tables, seq_lens, num_seqs, scale, out, out_dtype);
+  if (rc || num_seqs == 0) return rc;
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_err(e, "hipGetDevice");
+  if (dev != pool->device)
+    return set_err(KVP_EINVAL, "the current device is %d, the pool lives on device %d", dev, pool->device);
+  DecodeLayout L;
+  rc = layout_decode(pool, seq_lens, num_seqs, maxp, group_prefix, num_q_heads, &L);
+  if (rc) return rc;
+  const size_t meta_bytes = L.meta.size();
+  if (meta_bytes + L.total > kNoAllocScratchBytes)
+    return set_err(KVP_EWORKSPACE, "the call needs %zu bytes of scratch, more than the %zu of the allocation-free "
+                   "entry point", meta_bytes + L.total, kNoAllocScratchBytes);
+  unsigned char* sp = nullptr;
+  rc = scratch_of(dev, &sp);
+  if (rc) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  // [work list][partial accumulators][partial (m, l)]: the work list travels in launch arguments.
+  L.meta.buf.resize(meta_bytes, 0);
+  e = kvp::launch_put_bytes(sp, L.meta.buf.data(), meta_bytes, s);
+  if (e == hipSuccess)
+    e = launch_decode_plan(L, pool, layer, q, block_tables, maxp, num_q_heads, scale, out, out_dtype, sp,
+                           sp + meta_bytes, s);
+  return e == hipSuccess ? KVP_OK : hip_err(e, "paged_decode_attn_noalloc launch");
 }
 
 int prefix_chunk_prefill_workspace_size(kvp_pool_t pool, const int32_t* ctx_lens, const int32_t* cu_q, int num_seqs,

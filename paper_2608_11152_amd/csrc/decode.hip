@@ -11,6 +11,9 @@
 // head).  The score tile's register layout is exactly the layout of the P^T operand of the next product
 // O^T = V^T P^T (16 d-rows x 16 columns, k = 32 token slots of two pages), so probabilities never leave
 // registers.  The pool layout (kvp_layout.h) makes every K and V operand a contiguous 16-byte load.
+#include <algorithm>
+#include <cstring>
+
 #include "kvp_kernels.h"
 #include "kvp_layout.h"
 
@@ -768,7 +771,39 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(MergeArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------------------------------
+// Host bytes written to device memory through kernel arguments (the allocation-free decode entry point
+// stages its work list this way: no pinned host buffer, and the bytes travel by value with the launch).
+// ---------------------------------------------------------------------------------------------------
+constexpr int kArgChunkBytes = 3840;  // payload per launch; the whole argument block stays under 4 KB
+
+struct ArgChunk {
+  unsigned char* dst;
+  uint32_t n;  // payload bytes, a multiple of 16
+  uint32_t pad;
+  uint4 bytes[kArgChunkBytes / 16];
+};
+
+__global__ __launch_bounds__(256) void put_bytes_kernel(ArgChunk c) {
+  for (uint32_t i = threadIdx.x; i < c.n / 16; i += blockDim.x) reinterpret_cast<uint4*>(c.dst)[i] = c.bytes[i];
+}
+
 }  // namespace
+
+hipError_t launch_put_bytes(void* dst, const void* src, size_t n, hipStream_t s) {
+  const unsigned char* h = reinterpret_cast<const unsigned char*>(src);
+  for (size_t off = 0; off < n; off += kArgChunkBytes) {
+    ArgChunk c{};
+    const size_t k = std::min<size_t>(kArgChunkBytes, n - off);
+    c.dst = reinterpret_cast<unsigned char*>(dst) + off;
+    c.n = (uint32_t)((k + 15) & ~size_t(15));
+    std::memcpy(c.bytes, h + off, k);
+    hipLaunchKernelGGL(put_bytes_kernel, dim3(1), dim3(256), 0, s, c);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
 
 hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s) {
   const int64_t blocks = (int64_t)a.n_wave_blocks + a.n_group_blocks;

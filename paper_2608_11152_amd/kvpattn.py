@@ -22,7 +22,8 @@ PAGE = 16
 
 # Every symbol the header declares (kept in sync by a CPU test that parses include/kvpattn.h).
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_reset", "kv_pool_layer_ptr", "kv_pool_info",
-           "kv_pool_dtype", "kv_pool_set_scales", "kv_pool_device_error", "kv_append", "kv_gather", "paged_decode_workspace_size", "paged_decode_attn",
+           "kv_pool_dtype", "kv_pool_set_scales", "kv_pool_device_error", "kv_append", "kv_gather",
+           "paged_decode_workspace_size", "paged_decode_attn", "paged_decode_attn_noalloc",
            "prefix_chunk_prefill_workspace_size", "prefix_chunk_prefill_attn", "kv_pool_page_bytes", "kv_offload",
            "kv_restore", "kvp_block_hashes", "kvp_group_shared_pages", "kvp_prefix_table_create",
            "kvp_prefix_table_destroy", "kvp_prefix_table_clear", "kvp_prefix_table_insert", "kvp_prefix_table_erase",
@@ -66,6 +67,7 @@ def lib() -> C.CDLL:
         L.kv_gather.argtypes = [p, i, vp, i, i32p, i, vp, vp, vp]
         L.paged_decode_workspace_size.argtypes = [p, i32p, i, gpp, i, C.POINTER(sz)]
         L.paged_decode_attn.argtypes = [vp, p, i, vp, i, i32p, i, gpp, i, C.c_float, vp, i, vp, sz, vp]
+        L.paged_decode_attn_noalloc.argtypes = [vp, p, i, vp, i, i32p, i, gpp, i, C.c_float, vp, i, vp]
         L.prefix_chunk_prefill_workspace_size.argtypes = [p, i32p, i32p, i, i, C.POINTER(sz)]
         L.prefix_chunk_prefill_attn.argtypes = [vp, p, i, vp, i, i32p, i32p, i, i, C.c_float, vp, i, vp, sz, vp]
         L.kv_pool_page_bytes.argtypes = [p, C.POINTER(sz)]
@@ -346,6 +348,32 @@ def paged_decode_attn(q, pool: Pool, layer, block_tables, seq_lens, group_prefix
     _check(lib().paged_decode_attn(_dptr(q), pool.handle, layer, _dptr(block_tables), block_tables.shape[1],
                                    _ptr(sl), len(sl), _gp_ref(gpr), Hq, float(scale), _dptr(out), od, _dptr(ws),
                                    ws.numel() * ws.element_size(), _stream(stream)), "paged_decode_attn")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # KVP_NOALLOC_SCRATCH_BYTES
+
+
+def paged_decode_attn_noalloc(q, pool: Pool, layer, block_tables, seq_lens, out, group_prefix=None, scale=None,
+                              stream=None):
+    """paged_decode_attn through the allocation-free entry point: the caller passes `out`; the library
+    keeps the work list and partials in its own per-GPU scratch (calls that overlap on one GPU race)."""
+    import torch
+    sl = _i32(seq_lens)
+    _dev(q, "q", _bf16(), 3)
+    B, Hq, d = q.shape
+    _check_q_heads(q, pool)
+    if B != len(sl):
+        raise ValueError(f"q holds {B} sequences, seq_lens {len(sl)}")
+    _dev(block_tables, "block_tables", _i32t(), 2, rows=B)
+    _dev(out, "out", _outt(), 3, rows=B, tail=(Hq, d))
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    od = KVP_F32 if out.dtype == torch.float32 else KVP_BF16
+    gpr = group_prefix if not isinstance(group_prefix, tuple) else _GP(*group_prefix)
+    _check(lib().paged_decode_attn_noalloc(_dptr(q), pool.handle, layer, _dptr(block_tables), block_tables.shape[1],
+                                           _ptr(sl), len(sl), _gp_ref(gpr), Hq, float(scale), _dptr(out), od,
+                                           _stream(stream)), "paged_decode_attn_noalloc")
     return out
 
 
