@@ -97,3 +97,20 @@ def assert_close(got, ref, what, max_abs=MAX_ABS, mean_abs=MEAN_ABS):
     mx, mn = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
     note(f"{what}: max_abs={mx:.3e} mean_abs={mn:.3e}")
     assert mx <= max_abs and mn <= mean_abs, f"{what}: max_abs={mx:.3e} mean_abs={mn:.3e}"
+
+
+def oracle_by_kv_head(fn, q_bits, k_bits, v_bits, scale, *args, **kw):
+    """Call an oracle routine (oracle.decode_seq or oracle.prefill_seq) once per KV head on contiguous
+    copies of that head's K/V, with the query heads that read it (head h reads KV head h // (Hq / Hkv),
+    reading c-2).  The arithmetic per head is the single call's; only the strided gathers are avoided,
+    which makes the full-size comparisons several times faster.  q_bits [..., Hq, d] raw bf16;
+    k_bits, v_bits [n, Hkv, d] raw bf16 (or float64 values)."""
+    Hq, Hkv = q_bits.shape[-2], k_bits.shape[1]
+    G = Hq // Hkv
+    outs = []
+    for g in range(Hkv):
+        kg, vg = np.ascontiguousarray(k_bits[:, g:g + 1]), np.ascontiguousarray(v_bits[:, g:g + 1])
+        if kg.dtype == np.uint16:
+            kg, vg = oracle.widen_bf16(kg), oracle.widen_bf16(vg)
+        outs.append(fn(np.ascontiguousarray(q_bits[..., g * G:(g + 1) * G, :]), kg, vg, scale, *args, **kw))
+    return np.concatenate(outs, axis=-2)

@@ -1,6 +1,7 @@
 """Parity at the full workload sizes (RLVR 64x8, RLHF 128x2, agentic 32 x 32k-128k, mixed 40 sessions in a
 1.5M-token pool), in the launch configuration the benchmark times (same plan, bf16 output).  The oracle
-computes sampled outputs one sequence / one set of query rows at a time from the generator's values."""
+computes every decoding sequence, and the prefill rows named in each test, one sequence at a time from the
+generator's values."""
 import numpy as np
 import pytest
 
@@ -8,7 +9,7 @@ import oracle
 from paper_2608_11152_amd import kvpattn as kp
 from paper_2608_11152_amd import workloads as W
 
-from gpu_helpers import GpuCase, assert_close, note
+from gpu_helpers import GpuCase, assert_close, note, oracle_by_kv_head
 
 pytestmark = pytest.mark.gpu
 
@@ -52,6 +53,29 @@ def test_full_decode_sampled(full):
     assert np.all(np.isfinite(out))
 
 
+def test_full_decode_every_sequence(full):
+    """Every decoding sequence of the workload against the oracle (run per KV head on contiguous copies;
+    the first sequence also through the oracle's own all-head call, which must agree bitwise)."""
+    import time
+    import torch
+    c, w = full, full.w
+    note(f"full decode {w.name}: every sequence")
+    out = c.decode(out_dtype=torch.bfloat16).float().cpu().numpy().astype(np.float64)
+    assert c.pool.device_error() == kp.KVP_OK
+    q = W.to_numpy_bits(c.vals.q)
+    dec = np.flatnonzero(w.decode_len > 0)
+    t0 = time.time()
+    ref = np.zeros((len(dec), w.Hq, w.d))
+    for j, i in enumerate(dec):
+        kb, vb = W.seq_kv_bits(w, c.vals, int(i), int(w.decode_len[i]))
+        ref[j] = oracle_by_kv_head(oracle.decode_seq, q[i], kb, vb, w.scale)
+        if j == 0:
+            own = oracle.decode_seq(q[i], oracle.widen_bf16(kb), oracle.widen_bf16(vb), w.scale)
+            assert np.max(np.abs(ref[j] - own)) <= 1e-12
+    note(f"full decode {w.name}: oracle over {len(dec)} sequences took {time.time() - t0:.1f} s")
+    assert_close(out[dec], ref, f"full decode {w.name} (all {len(dec)} decoding sequences)")
+
+
 def test_full_append_sampled_bitwise(full):
     import torch
     c, w = full, full.w
@@ -68,7 +92,11 @@ def test_full_append_sampled_bitwise(full):
         off += n
 
 
-def test_full_prefill_sampled_rows(full):
+def test_full_prefill_rows(full):
+    """Every row of the session with the longest history; in every other session the first 32, the last
+    32 and a seeded block of 32 rows (rows are independent, so each is checked exactly as in the full
+    result).  One session's rows also go through the oracle's own all-head call."""
+    import time
     c, w = full, full.w
     if not len(w.prefill_seqs):
         pytest.skip("workload has no prefill chunk")
@@ -78,13 +106,26 @@ def test_full_prefill_sampled_rows(full):
     qp = W.to_numpy_bits(c.vals.qp)
     cu = w.cu_q()
     rng = np.random.default_rng(5)
-    for j in sorted({0, len(w.prefill_seqs) - 1, int(rng.integers(len(w.prefill_seqs)))}):
+    longest = int(np.argmax(w.prefill_ctx))
+    t0 = time.time()
+    for j in range(len(w.prefill_seqs)):
         C, ctx, seq = int(w.prefill_chunk[j]), int(w.prefill_ctx[j]), int(w.prefill_seqs[j])
-        rows = np.unique(np.r_[0:64, C - 64:C, rng.integers(0, C, 64)])
         k, v = W.seq_kv_bits(w, c.vals, seq, ctx + C)
-        ref = oracle.prefill_seq(qp[cu[j]:cu[j + 1]], oracle.widen_bf16(k), oracle.widen_bf16(v), w.scale, ctx,
-                                 rows=rows)
-        assert_close(out[cu[j] + rows], ref, f"full prefill {w.name} session {j} ({len(rows)} rows)")
+        if j == longest:
+            blocks = [(0, C)]
+        else:
+            mid = int(rng.integers(32, max(33, C - 64)))
+            blocks = [(0, min(32, C)), (mid, min(mid + 32, C)), (max(0, C - 32), C)]
+        for r0, r1 in blocks:
+            ref = oracle_by_kv_head(oracle.prefill_seq, qp[cu[j] + r0:cu[j] + r1], k, v, w.scale, ctx + r0)
+            if j == 0 and r0 == 0:
+                n_own = min(32, r1)
+                own = oracle.prefill_seq(qp[cu[j]:cu[j] + n_own], oracle.widen_bf16(k), oracle.widen_bf16(v), w.scale,
+                                         ctx)
+                assert np.max(np.abs(ref[:n_own] - own)) <= 1e-12
+            assert_close(out[cu[j] + r0:cu[j] + r1], ref,
+                         f"full prefill {w.name} session {j} rows {r0}..{r1 - 1} (ctx {ctx})")
+    note(f"full prefill {w.name}: oracle took {time.time() - t0:.1f} s")
 
 
 def test_full_mixed_fp8_decode_sampled():
