@@ -225,3 +225,15 @@ def test_product_code_never_imports_the_oracle():
             if f.endswith((".py", ".cpp", ".hip", ".h")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert not pat.search(text), os.path.join(dirpath, f)
+
+
+def test_product_code_never_imports_the_controller_replay():
+    """The MISA-T controller replay (misa_t/) is a harness around the library: the package never imports
+    it, and neither does the benchmark."""
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    pat = re.compile(r"^\s*(import\s+misa_t|from\s+misa_t\b)", re.M)
+    paths = [os.path.join(root, "bench.py")]
+    for dirpath, _, files in os.walk(os.path.join(root, "paper_2608_11152_amd")):
+        paths += [os.path.join(dirpath, f) for f in files if f.endswith(".py")]
+    for p in paths:
+        assert not pat.search(open(p).read()), p
