@@ -54,6 +54,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle baseline sample")
     ap.add_argument("--no-flush", action="store_true", help="do not evict the Infinity Cache between steps")
     ap.add_argument("--no-fp8", action="store_true", help="skip the FP8-KV leg (same step over an FP8 pool)")
+    ap.add_argument("--no-prefill-split", action="store_true",
+                    help="skip the split-history prefill leg (keeps a profile's prefill and merge kernels to the step)")
     return ap.parse_args()
 
 
@@ -517,7 +519,8 @@ def main():
         res["fp8_kv"]["decode_traffic"] = traffic["decode_fp8"]
         if has_prefill:
             res["fp8_kv"]["prefill_traffic"] = traffic["prefill_fp8"]
-    res["prefill_split"] = prefill_split_leg(kp, dev, stream)
+    if not args.no_prefill_split:
+        res["prefill_split"] = prefill_split_leg(kp, dev, stream)
     res["kv_tier"] = kv_tier_leg(kp, pool, w, stream)
     res["prefix_hash"] = prefix_hash_leg(kp, W, w, stream)
     if not args.no_cpu_baseline:
