@@ -319,9 +319,23 @@ int upload_runs(const std::vector<kvp::PageRun>& runs, hipStream_t s, void** dev
 // workspace holds [partial accumulators][partial (m, l)].
 struct DecodeLayout {
   kvp::DecodePlan plan;
-  Packer meta;
+  std::vector<int32_t> merge_info;  // one 16-byte record per merged sequence: {seq, first partial, count, 0}
   size_t off_wave = 0, off_seg = 0, off_group = 0, off_members = 0, off_part_base = 0, off_merge = 0;
+  size_t meta_bytes = 0;            // work list bytes (offsets above, 256-byte aligned)
   size_t off_acc = 0, off_ml = 0, total = 0;
+
+  // Copy the work list into `dst` (meta_bytes bytes), straight from the plan's arrays.
+  void write_meta(unsigned char* dst) const {
+    auto put = [&](size_t off, const void* src, size_t n) {
+      if (n) std::memcpy(dst + off, src, n);
+    };
+    put(off_wave, plan.wave_items.data(), plan.wave_items.size() * sizeof(kvp::DecodeItem));
+    put(off_seg, plan.seg_off.data(), plan.seg_off.size() * 4);
+    put(off_group, plan.group_items.data(), plan.group_items.size() * sizeof(kvp::DecodeItem));
+    put(off_members, plan.members.data(), plan.members.size() * 4);
+    put(off_part_base, plan.part_base.data(), plan.part_base.size() * 4);
+    put(off_merge, merge_info.data(), merge_info.size() * 4);
+  }
 };
 
 int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, const kvp_group_prefix* gp, int Hq,
@@ -329,29 +343,34 @@ int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, con
   kvp::Status st = kvp::plan_decode(seq_lens, B, maxp, gp, Hq, pool->num_kv_heads, &L->plan);
   if (!st.ok()) return from_status(st);
   const auto& P = L->plan;
-  L->off_wave = L->meta.add(P.wave_items.data(), P.wave_items.size() * sizeof(kvp::DecodeItem));
-  L->off_seg = L->meta.add(P.seg_off.data(), P.seg_off.size() * 4);
-  L->off_group = L->meta.add(P.group_items.data(), P.group_items.size() * sizeof(kvp::DecodeItem));
-  L->off_members = L->meta.add(P.members.data(), P.members.size() * 4);
-  L->off_part_base = L->meta.add(P.part_base.data(), P.part_base.size() * 4);
   // One 16-byte record per merged sequence, so a merge workgroup starts from a single read.
-  std::vector<int32_t> info(4 * P.merge_seqs.size());
+  L->merge_info.resize(4 * P.merge_seqs.size());
   for (size_t k = 0; k < P.merge_seqs.size(); ++k) {
     const int seq = P.merge_seqs[k];
-    info[4 * k] = seq;
-    info[4 * k + 1] = P.part_base[seq];
-    info[4 * k + 2] = P.n_parts[seq];
-    info[4 * k + 3] = 0;
+    L->merge_info[4 * k] = seq;
+    L->merge_info[4 * k + 1] = P.part_base[seq];
+    L->merge_info[4 * k + 2] = P.n_parts[seq];
+    L->merge_info[4 * k + 3] = 0;
   }
-  L->off_merge = L->meta.add(info.data(), info.size() * 4);
+  size_t at = 0;
+  auto slot = [&](size_t n) {
+    const size_t off = at;
+    at = (at + n + 255) & ~size_t(255);
+    return off;
+  };
+  L->off_wave = slot(P.wave_items.size() * sizeof(kvp::DecodeItem));
+  L->off_seg = slot(P.seg_off.size() * 4);
+  L->off_group = slot(P.group_items.size() * sizeof(kvp::DecodeItem));
+  L->off_members = slot(P.members.size() * 4);
+  L->off_part_base = slot(P.part_base.size() * 4);
+  L->off_merge = slot(L->merge_info.size() * 4);
+  L->meta_bytes = at;
   L->off_acc = 0;
   L->off_ml = L->off_acc + (((size_t)P.total_parts * Hq * pool->head_dim * 4 + 255) & ~size_t(255));
   L->total = L->off_ml + (((size_t)P.total_parts * Hq * 8 + 255) & ~size_t(255));
   return KVP_OK;
 }
 
-// Prefill: the caller's workspace holds the metadata (work list, lengths, split bookkeeping, one async
-// copy) followed by the partial states of split tiles [partial accumulators][partial (m, l)].
 // Launches the decode kernels (and the merge) for a laid-out plan whose metadata sits at `meta` (pinned
 // host memory or device memory) and whose partial states go to `part` (device memory of L.total bytes).
 hipError_t launch_decode_plan(const DecodeLayout& L, kvp_pool_t pool, int layer, const void* q,
@@ -413,6 +432,8 @@ int check_decode_args(kvp_pool_t pool, int layer, const void* q, const int32_t* 
   return KVP_OK;
 }
 
+// Prefill: the caller's workspace holds the metadata (work list, lengths, split bookkeeping, one async
+// copy) followed by the partial states of split tiles [partial accumulators][partial (m, l)].
 struct PrefillLayout {
   kvp::PrefillPlan plan;
   Packer meta;
@@ -971,9 +992,9 @@ int paged_decode_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* 
   // hundred KB, read once per wave), so no copy sits between the caller's previous work and the
   // decode kernels.  The slot is released after the last kernel that reads it.
   Staging::Lease lease;
-  rc = staging().lease(L.meta.buf.size(), &lease);
+  rc = staging().lease(L.meta_bytes, &lease);
   if (rc) return rc;
-  std::memcpy(lease.host, L.meta.buf.data(), L.meta.buf.size());
+  L.write_meta(reinterpret_cast<unsigned char*>(lease.host));
   hipError_t e = launch_decode_plan(L, pool, layer, q, block_tables, maxp, num_q_heads, scale, out, out_dtype,
                                     reinterpret_cast<const unsigned char*>(lease.host),
                                     reinterpret_cast<unsigned char*>(ws), s);
@@ -995,7 +1016,7 @@ int paged_decode_attn_noalloc(const void* q, kvp_pool_t pool, int layer, const i
   DecodeLayout L;
   rc = layout_decode(pool, seq_lens, num_seqs, maxp, group_prefix, num_q_heads, &L);
   if (rc) return rc;
-  const size_t meta_bytes = L.meta.size();
+  const size_t meta_bytes = L.meta_bytes;
   if (meta_bytes + L.total > kNoAllocScratchBytes)
     return set_err(KVP_EWORKSPACE, "the call needs %zu bytes of scratch, more than the %zu of the allocation-free "
                    "entry point", meta_bytes + L.total, kNoAllocScratchBytes);
@@ -1004,8 +1025,9 @@ int paged_decode_attn_noalloc(const void* q, kvp_pool_t pool, int layer, const i
   if (rc) return rc;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   // [work list][partial accumulators][partial (m, l)]: the work list travels in launch arguments.
-  L.meta.buf.resize(meta_bytes, 0);
-  e = kvp::launch_put_bytes(sp, L.meta.buf.data(), meta_bytes, s);
+  std::vector<unsigned char> meta(meta_bytes, 0);
+  L.write_meta(meta.data());
+  e = kvp::launch_put_bytes(sp, meta.data(), meta_bytes, s);
   if (e == hipSuccess)
     e = launch_decode_plan(L, pool, layer, q, block_tables, maxp, num_q_heads, scale, out, out_dtype, sp,
                            sp + meta_bytes, s);

@@ -70,21 +70,32 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
     return g >= 0 ? gp->shared_pages[g] : 0;
   };
 
-  // Members of each group that decode (seq_len > 0), in sequence order.
+  // Members of each group that decode (seq_len > 0), in sequence order: group g's are
+  // mem_list[mem_start[g] .. mem_start[g + 1]).
   const int NG = (gp ? gp->num_groups : 0);
-  std::vector<std::vector<int>> mem(NG);
+  std::vector<int> mem_start(NG + 1, 0), mem_list;
   for (int i = 0; i < B; ++i)
-    if (seq_lens[i] > 0 && shared_of(i) > 0) mem[gp->group_id[i]].push_back(i);
+    if (seq_lens[i] > 0 && shared_of(i) > 0) ++mem_start[gp->group_id[i] + 1];
+  for (int g = 0; g < NG; ++g) mem_start[g + 1] += mem_start[g];
+  mem_list.resize(mem_start[NG]);
+  {
+    std::vector<int> fill(mem_start.begin(), mem_start.end() - 1);
+    for (int i = 0; i < B; ++i)
+      if (seq_lens[i] > 0 && shared_of(i) > 0) mem_list[fill[gp->group_id[i]]++] = i;
+  }
+  auto n_mem = [&](int g) { return mem_start[g + 1] - mem_start[g]; };
 
   // Units: contiguous page ranges read for one set of query columns.  A group's shared prompt pages
   // form one unit per subgroup (at most 64 query columns, or 16 when wide groups go to the wave path,
   // see below), so the pages are read once per subgroup; each sequence's pages after its shared prefix
   // form one private unit.
+  // A unit's members (the sequences owning its query columns) are plan->members[mem_off, +n_mem): a
+  // group unit's are stored once and shared by all its chunks; a private unit's member is its row.
   struct Unit {
-    int kind, row, lo, hi, tok_end;
-    std::vector<int> mems;
+    int kind, row, lo, hi, tok_end, mem_off, n_mem;
   };
   std::vector<Unit> wave_units, group_units;
+  wave_units.reserve(B + NG);
   std::vector<int> group_unit_of(B, -1), wave_unit_of(B, -1);  // shared-prefix unit of each member
   // Groups wider than one wave's 16 columns normally take the LDS-staged path, whose 4-wave blocks keep
   // the whole call on 4-wave workgroups.  When reading their prompt pages once per 16-column subgroup
@@ -97,7 +108,7 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   for (int i = 0; i < B; ++i)
     if (seq_lens[i] > 0) call_pages += (seq_lens[i] + kPage - 1) / kPage - shared_of(i);
   for (int g = 0; g < NG; ++g) {
-    const int64_t m = (int64_t)mem[g].size(), S = gp->shared_pages[g];
+    const int64_t m = n_mem(g), S = gp->shared_pages[g];
     if (m == 0) continue;
     const int64_t n_group = (m + per_group_sub - 1) / per_group_sub, n_wave = (m + per_wave_sub - 1) / per_wave_sub;
     call_pages += n_group * S;
@@ -105,22 +116,27 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   }
   const bool wide_on_waves = extra_pages * 100 <= call_pages;
   const int per_sub = wide_on_waves ? per_wave_sub : per_group_sub;
+  plan->members.reserve(mem_list.size() + B);
   for (int g = 0; g < NG; ++g) {
-    if (mem[g].empty()) continue;
     const int S = gp->shared_pages[g];
-    for (size_t m0 = 0; m0 < mem[g].size(); m0 += per_sub) {
-      const size_t m1 = std::min(mem[g].size(), m0 + per_sub);
-      Unit u{1, mem[g][m0], 0, S, S * kPage, std::vector<int>(mem[g].begin() + m0, mem[g].begin() + m1)};
-      const bool wide = (int)u.mems.size() * G > kMaxColsPerWave;
-      for (int i : u.mems) (wide ? group_unit_of : wave_unit_of)[i] = (int)(wide ? group_units : wave_units).size();
-      (wide ? group_units : wave_units).push_back(std::move(u));
+    for (int m0 = mem_start[g]; m0 < mem_start[g + 1]; m0 += per_sub) {
+      const int m1 = std::min(mem_start[g + 1], m0 + per_sub);
+      Unit u{1, mem_list[m0], 0, S, S * kPage, (int)plan->members.size(), m1 - m0};
+      plan->members.insert(plan->members.end(), mem_list.begin() + m0, mem_list.begin() + m1);
+      const bool wide = u.n_mem * G > kMaxColsPerWave;
+      for (int k = m0; k < m1; ++k)
+        (wide ? group_unit_of : wave_unit_of)[mem_list[k]] = (int)(wide ? group_units : wave_units).size();
+      (wide ? group_units : wave_units).push_back(u);
     }
   }
   for (int i = 0; i < B; ++i) {
     if (seq_lens[i] <= 0) continue;
     const int lo = shared_of(i);
     const int hi = (seq_lens[i] + kPage - 1) / kPage;
-    if (hi > lo) wave_units.push_back(Unit{0, i, lo, hi, seq_lens[i], {i}});
+    if (hi > lo) {
+      wave_units.push_back(Unit{0, i, lo, hi, seq_lens[i], (int)plan->members.size(), 1});
+      plan->members.push_back(i);
+    }
   }
 
   // Wave-path units are cut into equal segments of consecutive pages ("stream-K" over the concatenated
@@ -152,6 +168,8 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   struct Chunk { int unit, lo, hi; };
   std::vector<Chunk> wave_chunks;
   std::vector<int> seg_of_chunk;
+  wave_chunks.reserve(wave_units.size() + segs_target + 1);
+  seg_of_chunk.reserve(wave_units.size() + segs_target + 1);
   std::vector<int> n_chunks_wave(wave_units.size(), 0);
   {
     int64_t fill = 0;
@@ -207,14 +225,15 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   plan->total_parts = total;
 
   auto emit = [&](const Unit& un, const Chunk& c, int k) {
-    DecodeItem it{un.kind, un.row, c.lo, c.hi, un.tok_end, (int)plan->members.size(), (int)un.mems.size(), 0};
-    plan->members.insert(plan->members.end(), un.mems.begin(), un.mems.end());
+    DecodeItem it{un.kind, un.row, c.lo, c.hi, un.tok_end, un.mem_off, un.n_mem, 0};
     if (un.kind == 1) it.slot = k;
     else it.slot = (n_prefix[un.row] == 0 && n_priv[un.row] == 1) ? -1 : n_prefix[un.row] + k;
     return it;
   };
   {
     std::vector<int> k_of(wave_units.size(), 0);
+    plan->seg_off.reserve(segs_target + 2);
+    plan->wave_items.reserve(wave_chunks.size());
     plan->seg_off.push_back(0);
     for (size_t c = 0; c < wave_chunks.size(); ++c) {
       if (c > 0 && seg_of_chunk[c] != seg_of_chunk[c - 1]) plan->seg_off.push_back((int)c);
