@@ -54,6 +54,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle baseline sample")
     ap.add_argument("--no-flush", action="store_true", help="do not evict the Infinity Cache between steps")
     ap.add_argument("--no-fp8", action="store_true", help="skip the FP8-KV leg (same step over an FP8 pool)")
+    ap.add_argument("--no-mixed-step", action="store_true",
+                    help="skip the leg that times the step's attention as one mixed_step_attn launch")
     ap.add_argument("--no-prefill-split", action="store_true",
                     help="skip the split-history prefill leg (keeps a profile's prefill and merge kernels to the step)")
     return ap.parse_args()
@@ -85,7 +87,8 @@ def prefill_algorithmic_bytes(w) -> int:
 
 PROFILE_OF = {"mixed": "decode_prefill_mixed_step.md", "rlvr": "decode_rlvr_64x8.md",
               "rlhf": "decode_rlhf_128x2.md", "agentic": "decode_prefill_agentic_32x128k.md"}
-KERNEL_SOURCES = ("decode.hip", "prefill.hip", "plan.cpp", "api.cpp", "kvp_layout.h", "kvp_kernels.h", "kvp_plan.h")
+KERNEL_SOURCES = ("decode.hip", "decode_dev.h", "prefill.hip", "prefill_dev.h", "plan.cpp", "api.cpp", "kvp_layout.h",
+                  "kvp_kernels.h", "kvp_plan.h")
 
 
 def profiled_traffic(workload: str) -> dict:
@@ -312,6 +315,52 @@ def prefill_split_leg(kp, dev, stream, ctx: int = 131072, chunks=(64, 256), reps
     return res
 
 
+def mixed_step_leg(kp, pool, w, vals, gp, bt, flush, stream, s0: int, s1: int, cu_q, reps: int = 10) -> dict:
+    """The step's attention (decode of every sequence and prefill of the chunks) as one mixed_step_attn
+    launch, against the two separate calls, on the same pool and inputs: runs interleaved, each after the
+    cache flush, timed with HIP events on the launch stream.  The outputs are compared bitwise."""
+    import torch
+    dev = vals.q.device
+    od = torch.empty((w.B, w.Hq, w.d), dtype=torch.bfloat16, device=dev)
+    op = torch.empty((int(cu_q[-1]), w.Hq, w.d), dtype=torch.bfloat16, device=dev)
+    rd, rp = torch.empty_like(od), torch.empty_like(op)
+    ws = torch.empty(max(1, kp.mixed_step_workspace_size(pool, w.decode_len, w.prefill_ctx, cu_q, w.Hq, gp)),
+                     dtype=torch.uint8, device=dev)
+    dws = torch.empty(max(1, kp.paged_decode_workspace_size(pool, w.decode_len, w.Hq, gp)), dtype=torch.uint8,
+                      device=dev)
+    pws = torch.empty(max(1, kp.prefix_chunk_prefill_workspace_size(pool, w.prefill_ctx, cu_q, w.Hq)),
+                      dtype=torch.uint8, device=dev)
+    btp = bt[s0:s1]
+
+    def fused():
+        kp.mixed_step_attn(pool, 0, vals.q, bt, w.decode_len, vals.qp, btp, w.prefill_ctx, cu_q, group_prefix=gp,
+                           scale=w.scale, out_dec=od, out_pf=op, ws=ws)
+
+    def separate():
+        kp.paged_decode_attn(vals.q, pool, 0, bt, w.decode_len, group_prefix=gp, scale=w.scale, out=rd, ws=dws)
+        kp.prefix_chunk_prefill_attn(vals.qp, pool, 0, btp, w.prefill_ctx, cu_q, scale=w.scale, out=rp, ws=pws)
+
+    t = {"fused": [], "separate": []}
+    for it in range(reps + 1):
+        for name, fn in (("separate", separate), ("fused", fused)):
+            flush.fill_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if it >= 1:
+                t[name].append(e0.elapsed_time(e1))
+    if pool.device_error() != kp.KVP_OK:
+        raise RuntimeError("device error in the mixed-step leg")
+    same = bool(torch.equal(od, rd) and torch.equal(op, rp))
+    f, sep = float(np.median(t["fused"])), float(np.median(t["separate"]))
+    return {"fused_ms": round(f, 4), "separate_ms": round(sep, 4), "speedup": round(sep / f, 4),
+            "fused_ms_p10_p90": [round(float(np.percentile(t["fused"], q)), 4) for q in (10, 90)],
+            "separate_ms_p10_p90": [round(float(np.percentile(t["separate"], q)), 4) for q in (10, 90)],
+            "outputs_bitwise_equal": same, "reps": reps}
+
+
 def cpu_baseline(w, vals, budget_s: float):
     """Time the CPU fp64 oracle (as it stands) on a bounded sample of the same decode workload."""
     import oracle
@@ -519,6 +568,8 @@ def main():
         res["fp8_kv"]["decode_traffic"] = traffic["decode_fp8"]
         if has_prefill:
             res["fp8_kv"]["prefill_traffic"] = traffic["prefill_fp8"]
+    if has_prefill and not args.no_mixed_step:
+        res["mixed_step"] = mixed_step_leg(kp, pool, w, vals, gp, bt, flush, stream, s0, s1, cu_q)
     if not args.no_prefill_split:
         res["prefill_split"] = prefill_split_leg(kp, dev, stream)
     res["kv_tier"] = kv_tier_leg(kp, pool, w, stream)

@@ -223,6 +223,34 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
                               size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------------------------
+ * mixed_step_attn — one launch for a serving step that decodes some sequences and prefills chunks of
+ * others on the same pool (Sec. 2.4 and Table 1: the rollout classes share one inference instance; the
+ * decode of Sec. 3.1 groups and the chunk prefill of Eq. 1 run side by side)
+ * ------------------------------------------------------------------------------------------------- */
+
+/* Workspace bytes mixed_step_attn needs (host arrays as below; either part may be empty). */
+int mixed_step_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int num_dec,
+                              const kvp_group_prefix* group_prefix, const int32_t* ctx_lens, const int32_t* cu_q,
+                              int num_pf, int num_q_heads, size_t* bytes);
+
+/* paged_decode_attn(q_dec, pool, layer, block_tables_dec, maxp_dec, seq_lens, num_dec, group_prefix,
+ * num_q_heads, scale, out_dec, out_dtype, ...) and prefix_chunk_prefill_attn(q_pf, pool, layer,
+ * block_tables_pf, maxp_pf, ctx_lens, cu_q, num_pf, num_q_heads, scale, out_pf, out_dtype, ...) in one
+ * kernel launch: the decode work is dispatched first and the prefill workgroups take the compute units as
+ * the decode's retire, so neither the decode's tail nor a launch boundary idles the GPU.  Split-KV
+ * partials of either part are merged by a second, small launch; shared-prefix ranges that the plan stages
+ * through LDS (wide groups over long prompts) run in a launch of their own ahead of the fused one; a call
+ * with one part empty makes that part's call.  Arguments, layouts and errors are those
+ * of the two calls (num_dec = 0 or num_pf = 0 leaves that part out); both parts read one pool and layer,
+ * and the prefill chunks' K/V must already have been appended.  Outputs are bitwise identical to the two
+ * calls.  ws: device workspace of ws_bytes >= mixed_step_workspace_size(...). */
+int mixed_step_attn(kvp_pool_t pool, int layer, int num_q_heads, float scale, int out_dtype, const void* q_dec,
+                    const int32_t* block_tables_dec, int maxp_dec, const int32_t* seq_lens, int num_dec,
+                    const kvp_group_prefix* group_prefix, void* out_dec, const void* q_pf,
+                    const int32_t* block_tables_pf, int maxp_pf, const int32_t* ctx_lens, const int32_t* cu_q,
+                    int num_pf, void* out_pf, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------------------------
  * CPU KV tier (Sec. 5.5: a host-memory tier keeps a backup copy of GPU-resident KV, so the GPU pool can
  * run close to capacity and pages evicted from it come back without recomputation)
  * ------------------------------------------------------------------------------------------------- */

@@ -20,7 +20,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_NAME = "libkvpattn.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 
-SOURCES = ["plan.cpp", "api.cpp", "append.hip", "decode.hip", "prefill.hip", "tier.hip", "prefix.hip"]
+SOURCES = ["plan.cpp", "api.cpp", "append.hip", "decode.hip", "prefill.hip", "mixed.hip", "tier.hip", "prefix.hip"]
 ARCH = "gfx950"
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result", f"-I{os.path.join(ROOT, 'include')}"]
 HIP_ONLY = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

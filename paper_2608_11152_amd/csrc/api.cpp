@@ -371,11 +371,11 @@ int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, con
   return KVP_OK;
 }
 
-// Launches the decode kernels (and the merge) for a laid-out plan whose metadata sits at `meta` (pinned
-// host memory or device memory) and whose partial states go to `part` (device memory of L.total bytes).
-hipError_t launch_decode_plan(const DecodeLayout& L, kvp_pool_t pool, int layer, const void* q,
-                              const int32_t* block_tables, int maxp, int num_q_heads, float scale, void* out,
-                              int out_dtype, const unsigned char* meta, unsigned char* part, hipStream_t s) {
+// Kernel arguments of a laid-out decode plan whose metadata sits at `meta` (pinned host memory or device
+// memory) and whose partial states go to `part` (device memory of L.total bytes).
+kvp::DecodeArgs decode_args(const DecodeLayout& L, kvp_pool_t pool, int layer, const void* q,
+                            const int32_t* block_tables, int maxp, int num_q_heads, float scale, void* out,
+                            int out_dtype, const unsigned char* meta, unsigned char* part) {
   const auto& P = L.plan;
   kvp::DecodeArgs a{};
   a.q = reinterpret_cast<const uint16_t*>(q);
@@ -403,19 +403,37 @@ hipError_t launch_decode_plan(const DecodeLayout& L, kvp_pool_t pool, int layer,
   a.n_group_items = (int)P.group_items.size();
   a.n_group_blocks = a.n_group_items * a.Hkv;
   a.n_wave_blocks = (a.n_items * a.Hkv + 3) / 4;
+  return a;
+}
+
+// The merge of split partials (decode: one record per split sequence; prefill: one per query row of a
+// split session), enqueued after the kernels that write the partials.
+hipError_t launch_merge(const int32_t* merge_info, int n_merge, const float* part_acc, const float2* part_ml,
+                        void* out, int out_f32, int num_q_heads, kvp_pool_t pool, hipStream_t s) {
+  if (n_merge == 0) return hipSuccess;
+  kvp::MergeArgs mg{};
+  mg.merge_info = merge_info;
+  mg.n_merge = n_merge;
+  mg.part_acc = part_acc;
+  mg.part_ml = part_ml;
+  mg.out = out;
+  mg.out_f32 = out_f32;
+  mg.Hq = num_q_heads;
+  mg.Hkv = pool->num_kv_heads;
+  return kvp::launch_decode_merge(mg, pool->head_dim, s);
+}
+
+// Launches the decode kernels (and the merge) for a laid-out plan (metadata and partials as in
+// decode_args).
+hipError_t launch_decode_plan(const DecodeLayout& L, kvp_pool_t pool, int layer, const void* q,
+                              const int32_t* block_tables, int maxp, int num_q_heads, float scale, void* out,
+                              int out_dtype, const unsigned char* meta, unsigned char* part, hipStream_t s) {
+  const kvp::DecodeArgs a = decode_args(L, pool, layer, q, block_tables, maxp, num_q_heads, scale, out, out_dtype,
+                                        meta, part);
   hipError_t e = kvp::launch_decode(a, pool->head_dim, s);
-  if (e == hipSuccess && !P.merge_seqs.empty()) {
-    kvp::MergeArgs mg{};
-    mg.merge_info = reinterpret_cast<const int32_t*>(meta + L.off_merge);
-    mg.n_merge = (int)P.merge_seqs.size();
-    mg.part_acc = a.part_acc;
-    mg.part_ml = a.part_ml;
-    mg.out = out;
-    mg.out_f32 = a.out_f32;
-    mg.Hq = num_q_heads;
-    mg.Hkv = pool->num_kv_heads;
-    e = kvp::launch_decode_merge(mg, pool->head_dim, s);
-  }
+  if (e == hipSuccess)
+    e = launch_merge(reinterpret_cast<const int32_t*>(meta + L.off_merge), (int)L.plan.merge_seqs.size(),
+                     a.part_acc, a.part_ml, out, a.out_f32, num_q_heads, pool, s);
   return e;
 }
 
@@ -455,6 +473,74 @@ int layout_prefill(kvp_pool_t pool, const int32_t* ctx_lens, const int32_t* cu_q
   L->off_acc = L->meta.size();
   L->off_ml = L->off_acc + (((size_t)P.total_parts * Hq * pool->head_dim * 4 + 255) & ~size_t(255));
   L->total = L->off_ml + (((size_t)P.total_parts * Hq * 8 + 255) & ~size_t(255));
+  return KVP_OK;
+}
+
+// Kernel arguments of a laid-out prefill plan whose metadata and partial states sit in the device
+// workspace `w` (metadata uploaded there first).
+kvp::PrefillArgs prefill_args(const PrefillLayout& L, kvp_pool_t pool, int layer, const void* q,
+                              const int32_t* block_tables, int maxp, int num_q_heads, float scale, void* out,
+                              int out_dtype, unsigned char* w) {
+  kvp::PrefillArgs a{};
+  a.q = reinterpret_cast<const uint16_t*>(q);
+  a.layer = layer_ptr(pool, layer);
+  a.bt = block_tables;
+  a.maxp = maxp;
+  a.items = reinterpret_cast<const kvp::PrefillItem*>(w + L.off_items);
+  a.n_items = (int)L.plan.items.size();
+  a.ctx_lens = reinterpret_cast<const int32_t*>(w + L.off_ctx);
+  a.cu_q = reinterpret_cast<const int32_t*>(w + L.off_cuq);
+  a.part_base = reinterpret_cast<const int32_t*>(w + L.off_part_base);
+  a.nsplit = reinterpret_cast<const int32_t*>(w + L.off_nsplit);
+  a.part_acc = reinterpret_cast<float*>(w + L.off_acc);
+  a.part_ml = reinterpret_cast<float2*>(w + L.off_ml);
+  a.out = out;
+  a.out_f32 = out_dtype == KVP_F32;
+  a.Hq = num_q_heads;
+  a.Hkv = pool->num_kv_heads;
+  a.G = num_q_heads / pool->num_kv_heads;
+  a.num_pages = pool->num_pages;
+  a.fp8 = pool->dtype == KVP_FP8_E4M3;
+  a.scale_log2 = scale * 1.4426950408889634f * (a.fp8 ? pool->k_scale[layer] : 1.0f);
+  a.v_scale = a.fp8 ? pool->v_scale[layer] : 1.0f;
+  a.err = pool->err;
+  return a;
+}
+
+// Checks of the prefill entry points (before anything is planned or enqueued).
+int check_prefill_args(kvp_pool_t pool, int layer, const void* q, const int32_t* block_tables,
+                       const int32_t* ctx_lens, const int32_t* cu_q, int num_seqs, float scale, const void* out,
+                       int out_dtype) {
+  int rc = check_layer(pool, layer);
+  if (rc) return rc;
+  if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
+  if (num_seqs == 0) return KVP_OK;
+  if (!q || !out || !block_tables || !ctx_lens || !cu_q) return set_err(KVP_EINVAL, "NULL pointer argument");
+  if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
+  if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
+  return KVP_OK;
+}
+
+// Workspace of a mixed step: [decode partials][prefill metadata + partials], each 256-byte aligned.
+struct MixedLayout {
+  DecodeLayout dec;
+  PrefillLayout pf;
+  size_t off_pf = 0, total = 0;
+};
+
+int layout_mixed(kvp_pool_t pool, int num_q_heads, const int32_t* seq_lens, int num_dec, int maxp_dec,
+                 const kvp_group_prefix* gp, const int32_t* ctx_lens, const int32_t* cu_q, int num_pf, int maxp_pf,
+                 MixedLayout* L) {
+  if (num_dec > 0) {
+    int rc = layout_decode(pool, seq_lens, num_dec, maxp_dec, gp, num_q_heads, &L->dec);
+    if (rc) return rc;
+  }
+  if (num_pf > 0) {
+    int rc = layout_prefill(pool, ctx_lens, cu_q, num_pf, maxp_pf, num_q_heads, &L->pf);
+    if (rc) return rc;
+  }
+  L->off_pf = (L->dec.total + 255) & ~size_t(255);
+  L->total = L->off_pf + (num_pf > 0 && L->pf.plan.real_items > 0 ? L->pf.total : 0);
   return KVP_OK;
 }
 
@@ -1047,13 +1133,8 @@ int prefix_chunk_prefill_workspace_size(kvp_pool_t pool, const int32_t* ctx_lens
 int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
                               const int32_t* ctx_lens, const int32_t* cu_q, int num_seqs, int num_q_heads, float scale,
                               void* out, int out_dtype, void* ws, size_t ws_bytes, void* stream) {
-  int rc = check_layer(pool, layer);
-  if (rc) return rc;
-  if (num_seqs < 0) return set_err(KVP_EINVAL, "num_seqs %d < 0", num_seqs);
-  if (num_seqs == 0) return KVP_OK;
-  if (!q || !out || !block_tables || !ctx_lens || !cu_q) return set_err(KVP_EINVAL, "NULL pointer argument");
-  if (out_dtype != KVP_BF16 && out_dtype != KVP_F32) return set_err(KVP_EUNSUPPORTED, "out_dtype %d", out_dtype);
-  if (!std::isfinite(scale) || !(scale > 0.0f)) return set_err(KVP_EINVAL, "scale must be finite and > 0");
+  int rc = check_prefill_args(pool, layer, q, block_tables, ctx_lens, cu_q, num_seqs, scale, out, out_dtype);
+  if (rc || num_seqs == 0) return rc;
   PrefillLayout L;
   rc = layout_prefill(pool, ctx_lens, cu_q, num_seqs, maxp, num_q_heads, &L);
   if (rc) return rc;
@@ -1064,44 +1145,94 @@ int prefix_chunk_prefill_attn(const void* q, kvp_pool_t pool, int layer, const i
   unsigned char* w = reinterpret_cast<unsigned char*>(ws);
   rc = staging().upload(w, L.meta.buf.data(), L.meta.buf.size(), s);
   if (rc) return rc;
-  kvp::PrefillArgs a{};
-  a.q = reinterpret_cast<const uint16_t*>(q);
-  a.layer = layer_ptr(pool, layer);
-  a.bt = block_tables;
-  a.maxp = maxp;
-  a.items = reinterpret_cast<const kvp::PrefillItem*>(w + L.off_items);
-  a.n_items = (int)L.plan.items.size();
-  a.ctx_lens = reinterpret_cast<const int32_t*>(w + L.off_ctx);
-  a.cu_q = reinterpret_cast<const int32_t*>(w + L.off_cuq);
-  a.part_base = reinterpret_cast<const int32_t*>(w + L.off_part_base);
-  a.nsplit = reinterpret_cast<const int32_t*>(w + L.off_nsplit);
-  a.part_acc = reinterpret_cast<float*>(w + L.off_acc);
-  a.part_ml = reinterpret_cast<float2*>(w + L.off_ml);
-  a.out = out;
-  a.out_f32 = out_dtype == KVP_F32;
-  a.Hq = num_q_heads;
-  a.Hkv = pool->num_kv_heads;
-  a.G = num_q_heads / pool->num_kv_heads;
-  a.num_pages = pool->num_pages;
-  a.fp8 = pool->dtype == KVP_FP8_E4M3;
-  a.scale_log2 = scale * 1.4426950408889634f * (a.fp8 ? pool->k_scale[layer] : 1.0f);
-  a.v_scale = a.fp8 ? pool->v_scale[layer] : 1.0f;
-  a.err = pool->err;
+  const kvp::PrefillArgs a = prefill_args(L, pool, layer, q, block_tables, maxp, num_q_heads, scale, out, out_dtype, w);
   hipError_t e = kvp::launch_prefill(a, pool->head_dim, s);
-  if (e == hipSuccess && !L.plan.merge_info.empty()) {
-    // split tiles: combine each query row's key ranges (the decode merge, one record per query row)
-    kvp::MergeArgs mg{};
-    mg.merge_info = reinterpret_cast<const int32_t*>(w + L.off_merge);
-    mg.n_merge = (int)(L.plan.merge_info.size() / 4);
-    mg.part_acc = a.part_acc;
-    mg.part_ml = a.part_ml;
-    mg.out = out;
-    mg.out_f32 = a.out_f32;
-    mg.Hq = num_q_heads;
-    mg.Hkv = pool->num_kv_heads;
-    e = kvp::launch_decode_merge(mg, pool->head_dim, s);
-  }
+  // split tiles: combine each query row's key ranges (the decode merge, one record per query row)
+  if (e == hipSuccess)
+    e = launch_merge(reinterpret_cast<const int32_t*>(w + L.off_merge), (int)(L.plan.merge_info.size() / 4),
+                     a.part_acc, a.part_ml, out, a.out_f32, num_q_heads, pool, s);
   return e == hipSuccess ? KVP_OK : hip_err(e, "prefix_chunk_prefill_attn launch");
+}
+
+int mixed_step_workspace_size(kvp_pool_t pool, const int32_t* seq_lens, int num_dec, const kvp_group_prefix* group_prefix,
+                              const int32_t* ctx_lens, const int32_t* cu_q, int num_pf, int num_q_heads,
+                              size_t* bytes) {
+  if (!pool_ok(pool) || !bytes) return set_err(KVP_EINVAL, "pool or bytes is NULL");
+  if (num_dec < 0 || num_pf < 0) return set_err(KVP_EINVAL, "negative sequence count");
+  MixedLayout L;
+  int rc = layout_mixed(pool, num_q_heads, seq_lens, num_dec, 1 << 28, group_prefix, ctx_lens, cu_q, num_pf, 1 << 28, &L);
+  if (rc) return rc;
+  *bytes = L.total;
+  return KVP_OK;
+}
+
+int mixed_step_attn(kvp_pool_t pool, int layer, int num_q_heads, float scale, int out_dtype, const void* q_dec,
+                    const int32_t* block_tables_dec, int maxp_dec, const int32_t* seq_lens, int num_dec,
+                    const kvp_group_prefix* group_prefix, void* out_dec, const void* q_pf,
+                    const int32_t* block_tables_pf, int maxp_pf, const int32_t* ctx_lens, const int32_t* cu_q,
+                    int num_pf, void* out_pf, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_decode_args(pool, layer, q_dec, block_tables_dec, seq_lens, num_dec, scale, out_dec, out_dtype);
+  if (rc) return rc;
+  rc = check_prefill_args(pool, layer, q_pf, block_tables_pf, ctx_lens, cu_q, num_pf, scale, out_pf, out_dtype);
+  if (rc) return rc;
+  MixedLayout L;
+  rc = layout_mixed(pool, num_q_heads, seq_lens, num_dec, maxp_dec, group_prefix, ctx_lens, cu_q, num_pf, maxp_pf, &L);
+  if (rc) return rc;
+  const bool has_pf = num_pf > 0 && L.pf.plan.real_items > 0;
+  if (num_dec == 0 && !has_pf) return KVP_OK;
+  if (L.total > 0 && (!ws || ws_bytes < L.total))
+    return set_err(KVP_EWORKSPACE, "workspace of %zu bytes, %zu needed", ws ? ws_bytes : (size_t)0, L.total);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  unsigned char* w = reinterpret_cast<unsigned char*>(ws);
+  kvp::DecodeArgs d{};
+  kvp::PrefillArgs p{};
+  Staging::Lease lease;
+  if (num_dec > 0) {
+    // the decode work list is read from a pinned staging slot, as in paged_decode_attn
+    rc = staging().lease(L.dec.meta_bytes, &lease);
+    if (rc) return rc;
+    L.dec.write_meta(reinterpret_cast<unsigned char*>(lease.host));
+    d = decode_args(L.dec, pool, layer, q_dec, block_tables_dec, maxp_dec, num_q_heads, scale, out_dec, out_dtype,
+                    reinterpret_cast<const unsigned char*>(lease.host), w);
+  }
+  hipError_t e = hipSuccess;
+  if (has_pf) {
+    rc = staging().upload(w + L.off_pf, L.pf.meta.buf.data(), L.pf.meta.buf.size(), s);
+    if (rc) {
+      if (num_dec > 0) (void)staging().release(lease, s, false);
+      return rc;
+    }
+    p = prefill_args(L.pf, pool, layer, q_pf, block_tables_pf, maxp_pf, num_q_heads, scale, out_pf, out_dtype,
+                     w + L.off_pf);
+  }
+  if (num_dec > 0 && !has_pf) {
+    e = kvp::launch_decode(d, pool->head_dim, s);                   // the decode call's own launch
+  } else if (num_dec == 0) {
+    e = kvp::launch_prefill(p, pool->head_dim, s);                  // the prefill call's own launch
+  } else {
+    // LDS-staged shared-prefix blocks (wide groups over long prompts) run in a launch of their own ahead
+    // of the fused one, which carries the wave-path blocks and the prefill blocks.
+    if (d.n_group_blocks > 0) {
+      kvp::DecodeArgs g = d;
+      g.n_wave_blocks = 0;
+      e = kvp::launch_decode(g, pool->head_dim, s);
+    }
+    kvp::DecodeArgs wv = d;
+    wv.n_group_blocks = 0;
+    if (e == hipSuccess) e = kvp::launch_mixed_step(wv, p, pool->head_dim, pool->dtype == KVP_FP8_E4M3, s);
+  }
+  if (e == hipSuccess && num_dec > 0)
+    e = launch_merge(reinterpret_cast<const int32_t*>(reinterpret_cast<const unsigned char*>(lease.host) +
+                                                      L.dec.off_merge),
+                     (int)L.dec.plan.merge_seqs.size(), d.part_acc, d.part_ml, out_dec, d.out_f32, num_q_heads,
+                     pool, s);
+  if (e == hipSuccess && has_pf)
+    e = launch_merge(reinterpret_cast<const int32_t*>(w + L.off_pf + L.pf.off_merge),
+                     (int)(L.pf.plan.merge_info.size() / 4), p.part_acc, p.part_ml, out_pf, p.out_f32, num_q_heads,
+                     pool, s);
+  const int rr = num_dec > 0 ? staging().release(lease, s, e == hipSuccess) : KVP_OK;
+  if (e != hipSuccess) return hip_err(e, "mixed_step_attn launch");
+  return rr;
 }
 
 int kvp_check_tables(const int32_t* block_tables_host, int maxp, const int32_t* lens, int num_seqs, int num_pages,

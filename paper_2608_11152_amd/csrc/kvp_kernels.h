@@ -167,6 +167,11 @@ hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s);
 hipError_t launch_put_bytes(void* dst, const void* src, size_t n, hipStream_t s);
 hipError_t launch_decode_merge(const MergeArgs& a, int D, hipStream_t s);
 hipError_t launch_prefill(const PrefillArgs& a, int D, hipStream_t s);
+// One launch of decode wave-path blocks followed by prefill blocks (mixed.hip; the decode's LDS-staged
+// prefix blocks are not part of it); the decode block count is padded to a multiple of 8 so each prefill
+// item keeps its planned XCD.
+hipError_t launch_mixed_step(const DecodeArgs& d, const PrefillArgs& p, int D, bool fp8, hipStream_t s);
+int mixed_step_decode_blocks(const DecodeArgs& d);
 hipError_t launch_tier(const TierArgs& a, bool restore, hipStream_t s);
 hipError_t launch_block_hash(const HashArgs& a, int n_chunks, hipStream_t s);
 hipError_t launch_group_lcp(const GroupLcpArgs& a, int n_groups, hipStream_t s);

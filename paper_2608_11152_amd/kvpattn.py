@@ -24,7 +24,8 @@ PAGE = 16
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_reset", "kv_pool_layer_ptr", "kv_pool_info",
            "kv_pool_dtype", "kv_pool_set_scales", "kv_pool_device_error", "kv_append", "kv_gather",
            "paged_decode_workspace_size", "paged_decode_attn", "paged_decode_attn_noalloc",
-           "prefix_chunk_prefill_workspace_size", "prefix_chunk_prefill_attn", "kv_pool_page_bytes", "kv_offload",
+           "prefix_chunk_prefill_workspace_size", "prefix_chunk_prefill_attn", "mixed_step_workspace_size",
+           "mixed_step_attn", "kv_pool_page_bytes", "kv_offload",
            "kv_restore", "kvp_block_hashes", "kvp_group_shared_pages", "kvp_prefix_table_create",
            "kvp_prefix_table_destroy", "kvp_prefix_table_clear", "kvp_prefix_table_insert", "kvp_prefix_table_erase",
            "kvp_prefix_lookup", "kvp_prefix_table_error", "kvp_check_tables",
@@ -70,6 +71,9 @@ def lib() -> C.CDLL:
         L.paged_decode_attn_noalloc.argtypes = [vp, p, i, vp, i, i32p, i, gpp, i, C.c_float, vp, i, vp]
         L.prefix_chunk_prefill_workspace_size.argtypes = [p, i32p, i32p, i, i, C.POINTER(sz)]
         L.prefix_chunk_prefill_attn.argtypes = [vp, p, i, vp, i, i32p, i32p, i, i, C.c_float, vp, i, vp, sz, vp]
+        L.mixed_step_workspace_size.argtypes = [p, i32p, i, gpp, i32p, i32p, i, i, C.POINTER(sz)]
+        L.mixed_step_attn.argtypes = [p, i, i, C.c_float, i, vp, vp, i, i32p, i, gpp, vp, vp, vp, i, i32p, i32p, i,
+                                      vp, vp, sz, vp]
         L.kv_pool_page_bytes.argtypes = [p, C.POINTER(sz)]
         L.kv_offload.argtypes = [p, i, i32p, i, vp, vp]
         L.kv_restore.argtypes = [p, i, vp, i32p, i, vp, i, i, i32p, i32p, vp]
@@ -411,6 +415,60 @@ def prefix_chunk_prefill_attn(q, pool: Pool, layer, block_tables, ctx_lens, cu_q
                                            _ptr(cl), _ptr(cq), len(cl), Hq, float(scale), _dptr(out), od, _dptr(ws),
                                            ws.numel() * ws.element_size(), _stream(stream)), "prefix_chunk_prefill_attn")
     return out
+
+
+def mixed_step_workspace_size(pool: Pool, seq_lens, ctx_lens, cu_q, num_q_heads, group_prefix=None) -> int:
+    sl, cl, cq = _i32(seq_lens), _i32(ctx_lens), _i32(cu_q)
+    n = C.c_size_t()
+    _check(lib().mixed_step_workspace_size(pool.handle, _ptr(sl), len(sl), _gp_ref(group_prefix), _ptr(cl), _ptr(cq),
+                                           len(cl), num_q_heads, C.byref(n)), "mixed_step_workspace_size")
+    return n.value
+
+
+def mixed_step_attn(pool: Pool, layer, q_dec, block_tables_dec, seq_lens, q_pf, block_tables_pf, ctx_lens, cu_q,
+                    group_prefix=None, scale=None, out_dec=None, out_pf=None, out_dtype=None, ws=None, stream=None):
+    """paged_decode_attn and prefix_chunk_prefill_attn of one step in one launch.  Either part may be
+    empty (q_dec with 0 rows / q_pf with 0 rows).  Returns (out_dec, out_pf)."""
+    import torch
+    sl, cl, cq = _i32(seq_lens), _i32(ctx_lens), _i32(cu_q)
+    if len(cq) != len(cl) + 1:
+        raise ValueError(f"cu_q has {len(cq)} entries, {len(cl) + 1} needed")
+    _dev(q_dec, "q_dec", _bf16(), 3)
+    _dev(q_pf, "q_pf", _bf16(), 3)
+    B, Hq, d = q_dec.shape
+    T = q_pf.shape[0]
+    _check_q_heads(q_dec, pool)
+    _check_q_heads(q_pf, pool)
+    if tuple(q_pf.shape[1:]) != (Hq, d):
+        raise ValueError(f"q_pf rows are {tuple(q_pf.shape[1:])}, q_dec rows {(Hq, d)}")
+    if B != len(sl):
+        raise ValueError(f"q_dec holds {B} sequences, seq_lens {len(sl)}")
+    if len(cl) and T != int(cq[-1]):
+        raise ValueError(f"q_pf holds {T} rows, cu_q ends at {int(cq[-1])}")
+    _dev(block_tables_dec, "block_tables_dec", _i32t(), 2, rows=B)
+    _dev(block_tables_pf, "block_tables_pf", _i32t(), 2, rows=len(cl))
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if out_dec is None:
+        out_dec = _alloc_on(stream, (B, Hq, d), out_dtype or (out_pf.dtype if out_pf is not None else torch.float32),
+                            q_dec.device)
+    if out_pf is None:
+        out_pf = _alloc_on(stream, (T, Hq, d), out_dec.dtype, q_pf.device)
+    _dev(out_dec, "out_dec", _outt(), 3, rows=B, tail=(Hq, d))
+    _dev(out_pf, "out_pf", _outt(), 3, rows=T, tail=(Hq, d))
+    if out_dec.dtype != out_pf.dtype:
+        raise ValueError(f"out_dec is {out_dec.dtype}, out_pf {out_pf.dtype}: one output dtype per call")
+    od = KVP_F32 if out_dec.dtype == torch.float32 else KVP_BF16
+    gpr = group_prefix if not isinstance(group_prefix, tuple) else _GP(*group_prefix)
+    if ws is None:
+        ws = _alloc_on(stream, max(1, mixed_step_workspace_size(pool, sl, cl, cq, Hq, gpr)), torch.uint8, q_dec.device)
+    _dev(ws, "ws", (ws.dtype,))
+    _check(lib().mixed_step_attn(pool.handle, layer, Hq, float(scale), od, _dptr(q_dec), _dptr(block_tables_dec),
+                                 block_tables_dec.shape[1], _ptr(sl), len(sl), _gp_ref(gpr), _dptr(out_dec),
+                                 _dptr(q_pf), _dptr(block_tables_pf), block_tables_pf.shape[1], _ptr(cl), _ptr(cq),
+                                 len(cl), _dptr(out_pf), _dptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "mixed_step_attn")
+    return out_dec, out_pf
 
 
 def kv_pool_page_bytes(pool: Pool) -> int:
