@@ -87,7 +87,7 @@ def prefill_algorithmic_bytes(w) -> int:
 
 PROFILE_OF = {"mixed": "decode_prefill_mixed_step.md", "rlvr": "decode_rlvr_64x8.md",
               "rlhf": "decode_rlhf_128x2.md", "agentic": "decode_prefill_agentic_32x128k.md"}
-KERNEL_SOURCES = ("decode.hip", "decode_dev.h", "prefill.hip", "prefill_dev.h", "plan.cpp", "api.cpp", "kvp_layout.h",
+KERNEL_SOURCES = ("decode.hip", "decode_dev.h", "prefill.hip", "prefill_dev.h", "prefill_body.inc", "plan.cpp", "api.cpp", "kvp_layout.h",
                   "kvp_kernels.h", "kvp_plan.h")
 
 

@@ -10,7 +10,7 @@
 // block waits for another; split-KV partials of both parts are merged by the log-sum-exp merge kernel
 // after this launch.
 //
-// The block bodies are the decode and prefill kernels' own (decode_dev.h, prefill_dev.h), so every
+// The block bodies are the decode and prefill kernels' own (decode_dev.h, prefill_body.inc), so every
 // output is bitwise identical to the two separate calls with the same plans.  The kernel carries the
 // prefill's register and LDS budget (two 4-wave workgroups per CU), which is also the wave path's
 // occupancy in its own launch (8 waves per CU).  The LDS-staged shared-prefix blocks are not compiled
@@ -28,7 +28,11 @@ template <int D, bool FP8>
 __global__ __launch_bounds__(256, 2) void mixed_step_kernel(DecodeArgs d, PrefillArgs p, int n_dec_blocks) {
   const int b = blockIdx.x;
   if (b >= n_dec_blocks) {
-    pf::prefill_block<D, FP8>(p, (unsigned)(b - n_dec_blocks));
+    using namespace pf;
+    const PrefillArgs& a = p;
+    const unsigned item = (unsigned)(b - n_dec_blocks);
+    unsigned char* lds = prefill_lds<D>();
+#include "prefill_body.inc"
     return;
   }
   if (b < d.n_wave_blocks) dec::decode_wave_block<D, FP8>(d, b);  // the rest is padding

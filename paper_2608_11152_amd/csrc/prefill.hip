@@ -17,9 +17,13 @@
 namespace kvp {
 namespace {
 
+using namespace pf;
+
 template <int D, bool FP8>
 __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
-  pf::prefill_block<D, FP8>(a, blockIdx.x);
+  __shared__ __attribute__((aligned(16))) unsigned char lds[PrefillLds<D>::bytes];
+  const unsigned item = blockIdx.x;
+#include "prefill_body.inc"
 }
 
 }  // namespace
