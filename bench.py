@@ -462,21 +462,15 @@ def main():
             kp.kv_append(pool, 0, k, v, bt, ab.start_pos, ab.cu_new, group_prefix=gp if ab.use_group_prefix else None)
         if ev:
             ev[1].record(stream)
-        h0 = time.perf_counter()
         kp.paged_decode_attn(vals.q, pool, 0, bt, w.decode_len, group_prefix=gp, scale=w.scale, out=dec_out,
                              ws=dec_ws)
-        h1 = time.perf_counter()
         if ev:
             ev[2].record(stream)
         if has_prefill:
             kp.prefix_chunk_prefill_attn(vals.qp, pool, 0, bt[s0:s1], w.prefill_ctx, cu_q, scale=w.scale,
                                          out=pf_out, ws=pf_ws)
-        h2 = time.perf_counter()
         if ev:
             ev[3].record(stream)
-            host_ms.append(((h1 - h0) * 1e3, (h2 - h1) * 1e3))
-
-    host_ms = []  # host time of each call: validation, planning, packing and launch (it returns before the GPU)
 
     for _ in range(args.warmup):
         step()
@@ -491,6 +485,24 @@ def main():
     err = pool.device_error()
     if err != kp.KVP_OK:
         raise RuntimeError(f"device error {err} during the benchmark")
+    # Host time of each call (validation, planning, packing, launch), from 5 back-to-back calls after a
+    # synchronisation: inside the timed loop the host runs ahead until the library's ring of 8 pinned
+    # staging slots is full and then waits there for earlier steps, so a call's time there measures the
+    # GPU, not the host.
+    def host_time(fn):
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(5):
+            h0 = time.perf_counter()
+            fn()
+            ts.append((time.perf_counter() - h0) * 1e3)
+        torch.cuda.synchronize()
+        return ts
+    host_dec = host_time(lambda: kp.paged_decode_attn(vals.q, pool, 0, bt, w.decode_len, group_prefix=gp,
+                                                      scale=w.scale, out=dec_out, ws=dec_ws))
+    host_pf = host_time(lambda: kp.prefix_chunk_prefill_attn(vals.qp, pool, 0, bt[s0:s1], w.prefill_ctx, cu_q,
+                                                             scale=w.scale, out=pf_out, ws=pf_ws)) if has_prefill else [0.0]
+    host_ms = [(host_dec[i], host_pf[min(i, len(host_pf) - 1)]) for i in range(len(host_dec))]
     t_app = np.array([e[0].elapsed_time(e[1]) for e in evs])
     t_dec = np.array([e[1].elapsed_time(e[2]) for e in evs])
     t_pf = np.array([e[2].elapsed_time(e[3]) for e in evs])

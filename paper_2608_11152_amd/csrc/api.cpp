@@ -64,8 +64,9 @@ int hip_err(hipError_t e, const char* what) {
 
 // Ring of pinned host staging slots.  A slot is reused only after the GPU work that last read it has
 // completed (its event), so consecutive calls do not wait on each other's GPU work.  A slot is either
-// the source of one asynchronous copy (`upload`) or, for small per-call metadata, read by the kernels
-// directly over the bus (`lease` ... `release`), which saves the copy engine's latency.
+// the source of one copy into device memory (`upload`: a small copy kernel on the caller's stream, not
+// the copy engine, whose hand-off to the compute queue measured 20-30 us per call) or, for metadata each
+// wave reads once, read by the kernels directly over the bus (`lease` ... `release`).
 class Staging {
  public:
   struct Lease {
@@ -126,10 +127,10 @@ class Staging {
     int rc = lease(n, &l);
     if (rc) return rc;
     std::memcpy(l.host, src, n);
-    hipError_t e = hipMemcpyAsync(dst, l.host, n, hipMemcpyHostToDevice, s);
+    hipError_t e = kvp::launch_copy_from_host(dst, l.host, n, s);
     if (e != hipSuccess) {
       release(l, s, false);
-      return hip_err(e, "hipMemcpyAsync(metadata)");
+      return hip_err(e, "metadata copy");
     }
     return release(l, s);
   }
@@ -306,13 +307,14 @@ int run_tier(kvp_pool_t pool, int layer, const std::vector<kvp::TierItem>& items
   return rr;
 }
 
-int upload_runs(const std::vector<kvp::PageRun>& runs, hipStream_t s, void** dev) {
-  *dev = nullptr;
-  if (runs.empty()) return KVP_OK;
+// Page runs of kv_append / kv_gather in a leased pinned slot: each wave reads its one 24-byte record
+// there, so no device buffer, copy or allocation sits in the stream ahead of the kernel.
+int lease_runs(const std::vector<kvp::PageRun>& runs, Staging::Lease* lease) {
   const size_t n = runs.size() * sizeof(kvp::PageRun);
-  hipError_t e = hipMallocAsync(dev, n, s);
-  if (e != hipSuccess) return set_err(KVP_ENOMEM, "hipMallocAsync(%zu): %s", n, hipGetErrorString(e));
-  return staging().upload(*dev, runs.data(), n, s);
+  int rc = staging().lease(n, lease);
+  if (rc) return rc;
+  std::memcpy(lease->host, runs.data(), n);
+  return KVP_OK;
 }
 
 // Decode: the work list lives in a pinned staging slot (read by the kernels directly); the caller's
@@ -707,15 +709,15 @@ int kv_append(kvp_pool_t pool, int layer, const void* k, const void* v, const in
   build_runs(start_pos, first.data(), cnt.data(), num_seqs, &runs);
   if (runs.empty()) return KVP_OK;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  void* druns = nullptr;
-  rc = upload_runs(runs, s, &druns);
+  Staging::Lease lease;
+  rc = lease_runs(runs, &lease);
   if (rc) return rc;
   kvp::AppendArgs a{};
   a.k = reinterpret_cast<const uint16_t*>(k);
   a.v = reinterpret_cast<const uint16_t*>(v);
   a.layer = const_cast<uint16_t*>(layer_ptr(pool, layer));
   a.bt = block_tables;
-  a.runs = reinterpret_cast<const kvp::PageRun*>(druns);
+  a.runs = reinterpret_cast<const kvp::PageRun*>(lease.host);
   a.n_runs = (int)runs.size();
   a.maxp = maxp;
   a.Hkv = pool->num_kv_heads;
@@ -725,8 +727,9 @@ int kv_append(kvp_pool_t pool, int layer, const void* k, const void* v, const in
   a.inv_scale_k = 1.0f / pool->k_scale[layer];
   a.inv_scale_v = 1.0f / pool->v_scale[layer];
   hipError_t e = kvp::launch_append(a, pool->head_dim, s);
-  (void)hipFreeAsync(druns, s);
-  return e == hipSuccess ? KVP_OK : hip_err(e, "kv_append launch");
+  const int rr = staging().release(lease, s, e == hipSuccess);
+  if (e != hipSuccess) return hip_err(e, "kv_append launch");
+  return rr;
 }
 
 int kv_gather(kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp, const int32_t* lens, int num_seqs,
@@ -750,15 +753,15 @@ int kv_gather(kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
   build_runs(zero.data(), first.data(), lens, num_seqs, &runs);
   if (runs.empty()) return KVP_OK;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  void* druns = nullptr;
-  rc = upload_runs(runs, s, &druns);
+  Staging::Lease lease;
+  rc = lease_runs(runs, &lease);
   if (rc) return rc;
   kvp::GatherArgs a{};
   a.k = reinterpret_cast<uint16_t*>(k_out);
   a.v = reinterpret_cast<uint16_t*>(v_out);
   a.layer = layer_ptr(pool, layer);
   a.bt = block_tables;
-  a.runs = reinterpret_cast<const kvp::PageRun*>(druns);
+  a.runs = reinterpret_cast<const kvp::PageRun*>(lease.host);
   a.n_runs = (int)runs.size();
   a.maxp = maxp;
   a.Hkv = pool->num_kv_heads;
@@ -768,8 +771,9 @@ int kv_gather(kvp_pool_t pool, int layer, const int32_t* block_tables, int maxp,
   a.scale_k = pool->k_scale[layer];
   a.scale_v = pool->v_scale[layer];
   hipError_t e = kvp::launch_gather(a, pool->head_dim, s);
-  (void)hipFreeAsync(druns, s);
-  return e == hipSuccess ? KVP_OK : hip_err(e, "kv_gather launch");
+  const int rr = staging().release(lease, s, e == hipSuccess);
+  if (e != hipSuccess) return hip_err(e, "kv_gather launch");
+  return rr;
 }
 
 int kv_pool_page_bytes(kvp_pool_t pool, size_t* bytes) {

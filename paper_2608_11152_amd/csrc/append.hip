@@ -244,6 +244,18 @@ __global__ void fill_zero_kernel(uint4* p, size_t n16) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) p[i] = make_uint4(0, 0, 0, 0);
 }
 
+// Copy n bytes from pinned host memory to device memory: 16-byte pieces read over the host link by the
+// threads of the grid, the last n mod 16 bytes by one thread.  It runs on the compute queue in stream
+// order, so the kernel after it needs no hand-off from the copy engine.
+__global__ __launch_bounds__(256) void copy_from_host_kernel(unsigned char* dst, const unsigned char* src, size_t n) {
+  const size_t n16 = n / 16;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
+    reinterpret_cast<uint4*>(dst)[i] = reinterpret_cast<const uint4*>(src)[i];
+  if (blockIdx.x == 0 && threadIdx.x == 0)
+    for (size_t i = n16 * 16; i < n; ++i) dst[i] = src[i];
+}
+
 }  // namespace
 
 hipError_t launch_append(const AppendArgs& a, int D, hipStream_t s) {
@@ -273,6 +285,14 @@ hipError_t launch_gather(const GatherArgs& a, int D, hipStream_t s) {
   } else {
     hipLaunchKernelGGL(gather_kernel<64>, grid, dim3(256), 0, s, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_from_host(void* dst, const void* src, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const unsigned blocks = (unsigned)std::min<size_t>(256, (n / 16 + 255) / 256 + 1);
+  hipLaunchKernelGGL(copy_from_host_kernel, dim3(blocks), dim3(256), 0, s, reinterpret_cast<unsigned char*>(dst),
+                     reinterpret_cast<const unsigned char*>(src), n);
   return hipGetLastError();
 }
 

@@ -161,6 +161,9 @@ struct TableArgs {
 hipError_t launch_append(const AppendArgs& a, int D, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, int D, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+// Copy n bytes from pinned host memory (src) to device memory (dst; 16-byte aligned, like src) with a
+// kernel on stream s.
+hipError_t launch_copy_from_host(void* dst, const void* src, size_t n, hipStream_t s);
 hipError_t launch_decode(const DecodeArgs& a, int D, hipStream_t s);
 // Copy n host bytes (n rounded up to 16; dst 16-byte aligned) to device memory on stream s through the
 // launch arguments of small kernels: asynchronous, and neither side needs an allocation.
