@@ -83,10 +83,11 @@ Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int max
 Status check_tables(const int32_t* bt, int maxp, const int32_t* lens, int B, int num_pages,
                     const kvp_group_prefix* gp);
 
-constexpr int kPrefillRows = 128;  // flattened query rows per prefill workgroup
+constexpr int kPrefillWaves = 8;                    // waves per prefill workgroup, 32 query rows each
+constexpr int kPrefillRows = 32 * kPrefillWaves;    // flattened query rows per prefill workgroup
 // A call whose tiles (x their 64-key stages) would not give about this many equal workgroups splits
-// tile histories into key ranges: two resident 64 KB-LDS workgroups per CU on 256 CUs.
-constexpr int kPrefillSplitTarget = 512;
+// tile histories into key ranges: the resident prefill workgroups of 256 CUs (8 waves per CU).
+constexpr int kPrefillSplitTarget = 256 * 8 / kPrefillWaves;
 constexpr int kPrefillMinSplitStages = 16;  // smallest key range of a split (1024 keys)
 
 }  // namespace kvp
