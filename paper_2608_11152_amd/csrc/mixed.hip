@@ -12,7 +12,7 @@
 //
 // The block bodies are the decode and prefill kernels' own (decode_dev.h, prefill_body.inc), so every
 // output is bitwise identical to the two separate calls with the same plans.  The kernel carries the
-// prefill's register and LDS budget (two 4-wave workgroups per CU), which is also the wave path's
+// prefill's register and LDS budget (one 8-wave workgroup per CU), which is also the wave path's
 // occupancy in its own launch (8 waves per CU).  The LDS-staged shared-prefix blocks are not compiled
 // into this kernel: with their code beside the other two the compiler schedules the prefill's stage
 // loop differently and the prefill part ran 2.5% slower (with only the wave path beside it, the stage
