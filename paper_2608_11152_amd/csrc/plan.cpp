@@ -270,41 +270,62 @@ Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int max
   // History split.  Long histories under few query tiles (a short uncached suffix over a long cached
   // prefix, Eq. 1) would leave most CUs idle: each tile streams its whole history alone.  When the
   // call's tiles are fewer than kPrefillSplitTarget, each tile's 64-key stages are cut into ranges of
-  // about T stages, T chosen so that the call holds about kPrefillSplitTarget ranges (at least
-  // kPrefillMinSplitStages stages each).  A range may start only at a stage whose first key every query
-  // row of the session sees (st * 64 <= ctx), so every range is non-empty for every row; the ranges of
-  // one session are shared by all its tiles and the last one runs to each tile's own last stage.
+  // about T stages.  T starts where the call would hold about kPrefillSplitTarget ranges (at least
+  // kPrefillMinSplitStages stages each) and grows until the ranges fit the resident workgroups in one
+  // round: a range past that would wait for a whole range to finish.  A range may start only at a stage
+  // whose first key every query row of the session sees (st * 64 <= ctx), so every range is non-empty
+  // for every row; the ranges of one session are shared by all its tiles and the last one runs to each
+  // tile's own last stage.
   auto tile_stages = [&](int i, int t) {
     const int64_t C = cu_q[i + 1] - cu_q[i];
     const int64_t last_row = std::min<int64_t>(C * G - 1, (int64_t)t * kPrefillRows + kPrefillRows - 1);
     return (int)((ctx_lens[i] + last_row / G + 1 + 63) / 64);
   };
+  auto n_tiles = [&](int i) { return (int)(((int64_t)(cu_q[i + 1] - cu_q[i]) * G + kPrefillRows - 1) / kPrefillRows); };
+  std::vector<std::vector<int>> bounds(B);  // split starts after 0, per session
+  auto split_with = [&](int64_t T) {        // bounds for ranges of about T stages; returns the range count
+    int64_t ranges = 0;
+    for (int i = 0; i < B; ++i) {
+      bounds[i].clear();
+      const int C = cu_q[i + 1] - cu_q[i];
+      if (C == 0) continue;
+      const int nst = tile_stages(i, 0);             // the session's shortest tile
+      const int max_start = ctx_lens[i] / 64;        // latest stage a range may start at
+      const int64_t want = (nst + T - 1) / T;
+      const int S = (int)std::min<int64_t>(want, (int64_t)max_start + 1);
+      for (int k = 1; k < S; ++k) {
+        const int b = std::min<int>(max_start, (int)((int64_t)k * nst / S));
+        if (b > (bounds[i].empty() ? 0 : bounds[i].back())) bounds[i].push_back(b);
+      }
+      ranges += (int64_t)n_tiles(i) * Hkv * ((int64_t)bounds[i].size() + 1);
+    }
+    return ranges;
+  };
   plan->nsplit.assign(B, 1);
   plan->part_base.assign(B, 0);
-  std::vector<std::vector<int>> bounds(B);  // split starts after 0, per session
   {
-    int64_t tiles_total = 0, work = 0;
+    int64_t tiles_total = 0, work = 0, longest_tile = 0;
     for (int i = 0; i < B; ++i) {
-      const int C = cu_q[i + 1] - cu_q[i];
-      const int nt = (int)(((int64_t)C * G + kPrefillRows - 1) / kPrefillRows);
+      const int nt = n_tiles(i);
       tiles_total += (int64_t)nt * Hkv;
-      for (int t = 0; t < nt; ++t) work += (int64_t)tile_stages(i, t) * Hkv;
+      for (int t = 0; t < nt; ++t) {
+        work += (int64_t)tile_stages(i, t) * Hkv;
+        longest_tile = std::max<int64_t>(longest_tile, tile_stages(i, t));
+      }
     }
     if (tiles_total > 0 && tiles_total < kPrefillSplitTarget) {
-      const int64_t T = std::max<int64_t>(kPrefillMinSplitStages, (work + kPrefillSplitTarget - 1) / kPrefillSplitTarget);
-      for (int i = 0; i < B; ++i) {
-        const int C = cu_q[i + 1] - cu_q[i];
-        if (C == 0) continue;
-        const int nst = tile_stages(i, 0);             // the session's shortest tile
-        const int max_start = ctx_lens[i] / 64;        // latest stage a range may start at
-        const int64_t want = (nst + T - 1) / T;
-        const int S = (int)std::min<int64_t>(want, (int64_t)max_start + 1);
-        for (int k = 1; k < S; ++k) {
-          const int b = std::min<int>(max_start, (int)((int64_t)k * nst / S));
-          if (b > (bounds[i].empty() ? 0 : bounds[i].back())) bounds[i].push_back(b);
+      int64_t lo = std::max<int64_t>(kPrefillMinSplitStages, (work + kPrefillSplitTarget - 1) / kPrefillSplitTarget);
+      // The range count does not grow with T and is tiles_total (< the target) once T covers every
+      // tile: the smallest T in [lo, longest_tile] that fits, by bisection.
+      if (split_with(lo) > kPrefillSplitTarget) {
+        int64_t hi = std::max(lo, longest_tile);
+        while (lo + 1 < hi) {
+          const int64_t mid = lo + (hi - lo) / 2;
+          (split_with(mid) > kPrefillSplitTarget ? lo : hi) = mid;
         }
-        plan->nsplit[i] = (int)bounds[i].size() + 1;
+        split_with(hi);
       }
+      for (int i = 0; i < B; ++i) plan->nsplit[i] = (int)bounds[i].size() + 1;
     }
   }
   int32_t parts = 0;
@@ -323,20 +344,20 @@ Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int max
 
   // Units = contiguous runs of query tiles of one (session, kv head, key range).  Tiles of a unit read
   // the same KV, so a unit is kept on one XCD (workgroup b runs on XCD b % 8) to share that XCD's L2.
-  // Units are spread over the 8 XCDs longest-first; within an XCD the heaviest units start first.
+  // Units are spread over the 8 XCDs longest-first; within an XCD the heaviest units start first.  When
+  // the whole call fits the resident workgroups (one round), no XCD may take more than its share of
+  // them: a unit that fits no XCD whole is dealt out tile by tile.
   struct Unit { int seq, kvh, t0, t1, k; double w; };
   std::vector<Unit> units;
   int64_t tiles_total = 0;
-  for (int i = 0; i < B; ++i)
-    tiles_total += ((int64_t)(cu_q[i + 1] - cu_q[i]) * G + kPrefillRows - 1) / kPrefillRows * Hkv * plan->nsplit[i];
+  for (int i = 0; i < B; ++i) tiles_total += (int64_t)n_tiles(i) * Hkv * plan->nsplit[i];
   const int64_t seg = std::max<int64_t>(1, tiles_total / 64);  // at least ~64 units to balance 8 XCDs
   auto range_of = [&](int i, int k, int t, int* lo, int* hi) {
     *lo = k == 0 ? 0 : bounds[i][k - 1];
     *hi = k + 1 < plan->nsplit[i] ? bounds[i][k] : tile_stages(i, t);
   };
   for (int i = 0; i < B; ++i) {
-    const int C = cu_q[i + 1] - cu_q[i];
-    const int nt = (int)(((int64_t)C * G + kPrefillRows - 1) / kPrefillRows);
+    const int nt = n_tiles(i);
     for (int h = 0; h < Hkv; ++h)
       for (int k = 0; k < plan->nsplit[i]; ++k)
         for (int t0 = 0; t0 < nt; t0 += (int)seg) {
@@ -354,17 +375,31 @@ Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int max
   std::iota(order.begin(), order.end(), 0);
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return units[a].w > units[b].w; });
   constexpr int kXcd = 8;
+  const bool one_round = tiles_total <= kPrefillSplitTarget;
+  const size_t cap = one_round ? (size_t)(kPrefillSplitTarget / kXcd) : SIZE_MAX;
   std::vector<std::vector<PrefillItem>> bins(kXcd);
   std::vector<double> load(kXcd, 0.0);
+  auto place = [&](int x, const Unit& un, int t) {
+    int lo, hi;
+    range_of(un.seq, un.k, t, &lo, &hi);
+    load[x] += hi - lo;
+    bins[x].push_back(PrefillItem{un.seq, un.kvh, t * kPrefillRows, lo, hi,
+                                  plan->nsplit[un.seq] == 1 ? -1 : un.k, {0, 0}});
+  };
+  // the least-loaded XCD with room for n more workgroups, or -1
+  auto pick = [&](size_t n) {
+    int best = -1;
+    for (int x = 0; x < kXcd; ++x)
+      if (bins[x].size() + n <= cap && (best < 0 || load[x] < load[best])) best = x;
+    return best;
+  };
   for (int u : order) {
-    const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-    load[x] += units[u].w;
     const Unit& un = units[u];
-    for (int t = un.t0; t < un.t1; ++t) {
-      int lo, hi;
-      range_of(un.seq, un.k, t, &lo, &hi);
-      bins[x].push_back(PrefillItem{un.seq, un.kvh, t * kPrefillRows, lo, hi,
-                                    plan->nsplit[un.seq] == 1 ? -1 : un.k, {0, 0}});
+    const int x = pick((size_t)(un.t1 - un.t0));
+    if (x >= 0) {
+      for (int t = un.t0; t < un.t1; ++t) place(x, un, t);
+    } else {
+      for (int t = un.t0; t < un.t1; ++t) place(pick(1), un, t);  // total <= kXcd * cap: room for one
     }
   }
   size_t longest = 0;

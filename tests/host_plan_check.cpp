@@ -7,6 +7,8 @@
 //            partial slot of a sequence is written exactly once, segments never exceed the split size;
 //   prefill: every (session, KV head, query row) is covered exactly once per key range, the key ranges
 //            of a tile tile [0, its last key] without gaps or overlaps;
+//            a split call, and any call of at most one round, keeps every XCD within its share of the
+//            resident workgroups;
 //   both:    plans are deterministic, and invalid inputs return the documented error codes.
 // `self-test` plants mistakes into plans and expects the checks to reject each of them.
 #include <algorithm>
@@ -131,6 +133,17 @@ static bool check_prefill(const PrefillCase& c, const PrefillPlan& P) {
     if (it.slot >= 0) EXPECT(it.st_hi > it.st_lo, "empty split");
   }
   EXPECT(real == P.real_items, "real items %lld vs %lld", (long long)real, (long long)P.real_items);
+  {
+    // A split history is cut into few enough ranges that the whole call is one round of the resident
+    // workgroups, and a call that fits one round keeps every XCD (workgroup b on XCD b % 8) within its
+    // share of them: the padded grid is at most kPrefillSplitTarget long.
+    bool split = false;
+    for (int32_t n : P.nsplit) split |= n > 1;
+    if (split) EXPECT(P.real_items <= kvp::kPrefillSplitTarget, "split call of %lld workgroups", (long long)P.real_items);
+    if (P.real_items <= kvp::kPrefillSplitTarget)
+      EXPECT(P.items.size() <= (size_t)kvp::kPrefillSplitTarget, "one-round call padded to %zu workgroups",
+             P.items.size());
+  }
   {
     // every query row of a split session has nsplit partials of its own, in one merge record
     int32_t parts = 0;
@@ -356,6 +369,19 @@ static bool self_test() {
       if (!check_prefill(pc, b)) ++rejected;
       break;
     }
+  {
+    // one XCD given a workgroup past its share of the round
+    PrefillPlan b = Q;
+    size_t last = 0;
+    for (size_t j = 0; j < b.items.size(); ++j)
+      if (b.items[j].seq >= 0) last = j;
+    const PrefillItem moved = b.items[last];
+    b.items[last].seq = -1;
+    b.items.resize((size_t)kvp::kPrefillSplitTarget + 8, PrefillItem{-1, 0, 0, 0, 0, -1, {0, 0}});
+    b.items[(size_t)kvp::kPrefillSplitTarget + last % 8] = moved;
+    ++planted;
+    if (!check_prefill(pc, b)) ++rejected;
+  }
   std::printf("self-test: %d of %d planted mistakes rejected\n", rejected, planted);
   return planted > 0 && rejected == planted;
 }

@@ -40,16 +40,14 @@ def long_seq():
 
 
 def _rows(C, rng):
-    """Rows the oracle checks: all of them up to 64, else the first 32, the last 32 and 32 in between."""
-    if C <= 64:
+    """Rows the oracle checks: all of them up to 128, else the first 32, the last 32 and 32 in between."""
+    if C <= 128:
         return [np.arange(C)]
     mid = int(rng.integers(32, C - 64))
     return [np.arange(32), np.arange(mid, mid + 32), np.arange(C - 32, C)]
 
 
-@pytest.mark.parametrize("ctx", [32768, 131072])
-@pytest.mark.parametrize("C", [1, 16, 64, 256])
-def test_split_history_single_session(long_seq, ctx, C):
+def _check_single_session(long_seq, ctx, C):
     import torch
     pool, btd, k64, v64 = long_seq
     rng = np.random.default_rng(ctx + C)
@@ -65,6 +63,21 @@ def test_split_history_single_session(long_seq, ctx, C):
         j0 = int(rows[0])
         ref = oracle.prefill_seq(qb[j0:j0 + len(rows)], k64, v64, 0.088, ctx + j0)
         assert_close(o[rows], ref, f"split prefill ctx={ctx} C={C} rows {j0}..{j0 + len(rows) - 1}")
+
+
+@pytest.mark.parametrize("ctx", [32768, 131072])
+@pytest.mark.parametrize("C", [1, 16, 64, 256])
+def test_split_history_single_session(long_seq, ctx, C):
+    _check_single_session(long_seq, ctx, C)
+
+
+@pytest.mark.parametrize("ctx,C", [(32768, 96), (32768, 192)])
+def test_split_history_one_round(long_seq, ctx, C):
+    """Chunks of 3 and of 6 tiles per KV head over 32k cached keys.  Shares by work alone gave one XCD 33
+    of 252 workgroups (C = 96), and the first range length 264 workgroups (C = 192): a second round for a
+    few of them.  The planner now deals workgroups out within each XCD's 32 CUs and lengthens the ranges
+    until the call fits one round."""
+    _check_single_session(long_seq, ctx, C)
 
 
 def test_split_and_unsplit_sessions_in_one_call():
