@@ -276,12 +276,19 @@ Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int max
   // whose first key every query row of the session sees (st * 64 <= ctx), so every range is non-empty
   // for every row; the ranges of one session are shared by all its tiles and the last one runs to each
   // tile's own last stage.
-  auto tile_stages = [&](int i, int t) {
-    const int64_t C = cu_q[i + 1] - cu_q[i];
-    const int64_t last_row = std::min<int64_t>(C * G - 1, (int64_t)t * kPrefillRows + kPrefillRows - 1);
-    return (int)((ctx_lens[i] + last_row / G + 1 + 63) / 64);
-  };
   auto n_tiles = [&](int i) { return (int)(((int64_t)(cu_q[i + 1] - cu_q[i]) * G + kPrefillRows - 1) / kPrefillRows); };
+  // 64-key stages of every tile (its last row's keys), computed once: tile t of session i at tile_off[i] + t
+  std::vector<int64_t> tile_off(B + 1, 0);
+  for (int i = 0; i < B; ++i) tile_off[i + 1] = tile_off[i] + n_tiles(i);
+  std::vector<int> tile_st(tile_off[B]);
+  for (int i = 0; i < B; ++i) {
+    const int64_t C = cu_q[i + 1] - cu_q[i];
+    for (int t = 0; t < n_tiles(i); ++t) {
+      const int64_t last_row = std::min<int64_t>(C * G - 1, (int64_t)t * kPrefillRows + kPrefillRows - 1);
+      tile_st[tile_off[i] + t] = (int)((ctx_lens[i] + last_row / G + 1 + 63) / 64);
+    }
+  }
+  auto tile_stages = [&](int i, int t) { return tile_st[tile_off[i] + t]; };
   std::vector<std::vector<int>> bounds(B);  // split starts after 0, per session
   auto split_with = [&](int64_t T) {        // bounds for ranges of about T stages; returns the range count
     int64_t ranges = 0;
@@ -378,6 +385,7 @@ Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int max
   const bool one_round = tiles_total <= kPrefillSplitTarget;
   const size_t cap = one_round ? (size_t)(kPrefillSplitTarget / kXcd) : SIZE_MAX;
   std::vector<std::vector<PrefillItem>> bins(kXcd);
+  for (auto& b : bins) b.reserve((size_t)(tiles_total / kXcd + seg + 1));
   std::vector<double> load(kXcd, 0.0);
   auto place = [&](int x, const Unit& un, int t) {
     int lo, hi;
