@@ -407,7 +407,10 @@ Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int max
     if (x >= 0) {
       for (int t = un.t0; t < un.t1; ++t) place(x, un, t);
     } else {
-      for (int t = un.t0; t < un.t1; ++t) place(pick(1), un, t);  // total <= kXcd * cap: room for one
+      for (int t = un.t0; t < un.t1; ++t) {
+        const int y = pick(1);  // total <= kXcd * cap: some XCD has room for one
+        place(y >= 0 ? y : (int)(std::min_element(load.begin(), load.end()) - load.begin()), un, t);
+      }
     }
   }
   size_t longest = 0;
