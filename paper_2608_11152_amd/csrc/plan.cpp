@@ -143,8 +143,9 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   // unit list): segment s is processed by waves s*Hkv .. s*Hkv+Hkv-1 (one per KV head), so every wave
   // streams the same number of pages whatever the length skew, and a sequence is split only where a
   // segment boundary falls inside it.  About kDecodeWaves waves: one round of the waves that
-  // are resident at once on 256 CUs.  Segments hold at least 32 pages (512 tokens) so that a chunk's
-  // partial (G x d fp32 written, then read by the merge) stays within ~2% of its KV bytes.
+  // are resident at once on 256 CUs.  Segments hold at least 8 pages (128 tokens): a chunk's partial
+  // (G x d fp32 written, then read by the merge) stays within ~6% of its KV bytes, and a call too small
+  // for the budget (a few long sequences) still spreads over many waves instead of a few long ones.
   int64_t total_pages = 0, group_pages = 0;
   for (const Unit& u : wave_units) total_pages += u.hi - u.lo;
   for (const Unit& u : group_units) group_pages += u.hi - u.lo;

@@ -395,8 +395,9 @@ def test_host_errors_enqueue_nothing(cases):
     with pytest.raises(kp.KvpError) as e:
         kp.paged_decode_attn(q, c.pool, 0, c.bt, too_long, out=sentinel)
     assert e.value.code == kp.KVP_ERANGE
-    # a workload with partials needs workspace; the tiny one (one split per sequence) needs none
-    assert kp.paged_decode_workspace_size(c.pool, w.decode_len, w.Hq) == 0
+    # a call whose sequences fit one wave segment (8 pages in all) has no partials and needs no
+    # workspace; a workload with partials needs one
+    assert kp.paged_decode_workspace_size(c.pool, np.array([16, 30, 60, 1], np.int32), w.Hq) == 0
     cr = get_case(cases, "rlvr_s")
     need = kp.paged_decode_workspace_size(cr.pool, cr.w.decode_len, cr.w.Hq, cr.gp)
     assert need > 8
