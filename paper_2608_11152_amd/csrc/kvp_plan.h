@@ -88,6 +88,6 @@ constexpr int kPrefillRows = 32 * kPrefillWaves;    // flattened query rows per 
 // A call whose tiles (x their 64-key stages) would not give about this many equal workgroups splits
 // tile histories into key ranges: the resident prefill workgroups of 256 CUs (8 waves per CU).
 constexpr int kPrefillSplitTarget = 256 * 8 / kPrefillWaves;
-constexpr int kPrefillMinSplitStages = 16;  // smallest key range of a split (1024 keys)
+constexpr int kPrefillMinSplitStages = 8;  // smallest key range of a split (512 keys)
 
 }  // namespace kvp
