@@ -384,6 +384,42 @@ def test_decode_edge_lengths(G, d):
     assert np.all(out[0].cpu().numpy() == 0) and np.all(out[11].cpu().numpy() == 0)
 
 
+@pytest.mark.parametrize("lens", [[32773], [32773, 0, 16001]])
+def test_decode_few_long_sequences_many_partials(lens):
+    """A call of a few long sequences is cut into short (8-page) segments to fill the GPU: one 32k-token
+    sequence alone becomes hundreds of partials per KV head, all folded by the merge."""
+    import torch
+    Hq, Hkv, d = 32, 4, 128
+    _, parts, seg = kp.kvp_plan_decode(np.array(lens, np.int32), Hq, Hkv)
+    assert seg == 8 and parts >= 200, (parts, seg)
+    rng = np.random.default_rng(sum(lens))
+    pages = [(n + 15) // 16 for n in lens]
+    num_pages = sum(pages) + 3
+    perm = rng.permutation(num_pages).astype(np.int32)
+    bt = np.full((len(lens), max(pages)), -1, np.int32)
+    o = 0
+    for i, pg in enumerate(pages):
+        bt[i, :pg] = perm[o:o + pg]
+        o += pg
+    T = sum(lens)
+    kvb = W.f32_to_bf16_bits(rng.standard_normal((T, 2, Hkv, d), dtype=np.float32))
+    qb = W.f32_to_bf16_bits(rng.standard_normal((len(lens), Hq, d), dtype=np.float32))
+    pool = kp.Pool(1, num_pages, Hkv, d)
+    btd = torch.from_numpy(bt).cuda()
+    kvd = to_dev_bits(kvb)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    note(f"decode few long sequences {lens}: {parts} partials")
+    kp.kv_append(pool, 0, kvd[:, 0].contiguous(), kvd[:, 1].contiguous(), btd, np.zeros(len(lens), np.int32), cu)
+    out = kp.paged_decode_attn(to_dev_bits(qb), pool, 0, btd, lens, scale=0.0884)
+    torch.cuda.synchronize()
+    assert pool.device_error() == kp.KVP_OK
+    pk, pv = oracle.new_pool(num_pages, Hkv, d)
+    oracle.append(pk, pv, kvb[:, 0], kvb[:, 1], bt, np.zeros(len(lens), np.int32), cu)
+    ref = oracle.decode(qb, pk, pv, bt, lens, 0.0884)
+    assert_close(out, ref, f"few long sequences {lens}")
+    pool.close()
+
+
 def test_host_errors_enqueue_nothing(cases):
     import torch
     c = get_case(cases, "tiny")
