@@ -1,8 +1,9 @@
 """Chunked prefill whose tiles are too few to fill the GPU (a short uncached suffix over a long cached
 history, Eq. 1): the planner splits each tile's history into key ranges, every range writes a partial
 softmax state and the log-sum-exp merge combines them per query row.  Compared with the CPU fp64 oracle on
-one session with 32k and 128k cached tokens and chunks of 1 to 256 rows, on a batch mixing split and
-unsplit sessions, on an FP8 pool, with bf16 output, and for run-to-run determinism."""
+one session with 32k and 128k cached tokens and chunks of 1 to 256 rows, at other GQA ratios and head
+dims, on a batch mixing split and unsplit sessions, on an FP8 pool, with bf16 output, and for run-to-run
+determinism."""
 import numpy as np
 import pytest
 
@@ -78,6 +79,34 @@ def test_split_history_one_round(long_seq, ctx, C):
     few of them.  The planner now deals workgroups out within each XCD's 32 CUs and lengthens the ranges
     until the call fits one round."""
     _check_single_session(long_seq, ctx, C)
+
+
+@pytest.mark.parametrize("G,Hkv,d,ctx,C", [(1, 4, 64, 20000, 40), (4, 2, 64, 30000, 7), (16, 2, 128, 25000, 17),
+                                             (2, 8, 128, 9000, 100)])
+def test_split_history_other_gqa_ratios(G, Hkv, d, ctx, C):
+    """Split histories where C x G rows fill a 256-row tile only partly (G = 1, 4) or several times
+    over (G = 16), at both head dims, with ragged chunk and history lengths."""
+    import torch
+    Hq = G * Hkv
+    rng = np.random.default_rng(G * 1000 + C)
+    n = ctx + C
+    npg = (n + 15) // 16
+    num_pages = npg + 5
+    bt = rng.permutation(num_pages)[:npg].astype(np.int32)[None, :]
+    kvb = W.f32_to_bf16_bits(rng.standard_normal((n, 2, Hkv, d), dtype=np.float32))
+    qb = W.f32_to_bf16_bits(rng.standard_normal((C, Hq, d), dtype=np.float32))
+    pool = kp.Pool(1, num_pages, Hkv, d)
+    assert kp.prefix_chunk_prefill_workspace_size(pool, [ctx], [0, C], Hq) > 0, "expected a split history"
+    btd = torch.from_numpy(bt).cuda()
+    kvd = to_dev_bits(kvb)
+    note(f"prefill split G={G} Hkv={Hkv} d={d} ctx={ctx} C={C}")
+    kp.kv_append(pool, 0, kvd[:, 0].contiguous(), kvd[:, 1].contiguous(), btd, [0], [0, n])
+    out = kp.prefix_chunk_prefill_attn(to_dev_bits(qb), pool, 0, btd, [ctx], [0, C], scale=1.0 / np.sqrt(d))
+    torch.cuda.synchronize()
+    assert pool.device_error() == kp.KVP_OK
+    ref = oracle.prefill_seq(qb, oracle.widen_bf16(kvb[:, 0]), oracle.widen_bf16(kvb[:, 1]), 1.0 / np.sqrt(d), ctx)
+    assert_close(out, ref, f"split prefill G={G} d={d} ctx={ctx} C={C}")
+    pool.close()
 
 
 def test_split_and_unsplit_sessions_in_one_call():
