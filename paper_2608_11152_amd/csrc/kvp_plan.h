@@ -13,6 +13,7 @@ constexpr int kPage = 16;
 constexpr int kMaxColsPerWave = 16;   // query columns one wave's MFMA tile holds (members x heads)
 constexpr int kMaxColsPerGroup = 64;  // query columns one shared-prefix workgroup holds (4 waves)
 constexpr int kMinSegmentPages = 8;   // smallest page count of a decode wave segment
+constexpr int kChunkStartPages = 3;   // a wave chunk's start (item, query and first page ids), in pages
 constexpr int kGroupChunkPages = 16;  // pages per workgroup of the LDS-staged shared-prefix kernel
 // Decode waves per call: one round of the waves resident at once on 256 CUs (4 SIMDs x 2 waves each).
 // Sweeps of 1024-16384 put the optimum here on the target workloads.

@@ -164,7 +164,6 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   const int64_t segs_target = std::max<int64_t>(1, (budget_blocks - reserve) * 4 / Hkv);
   int64_t seg_pages = (total_pages + segs_target - 1) / segs_target;
   seg_pages = std::max<int64_t>(kMinSegmentPages, (seg_pages + 1) & ~int64_t(1));
-  plan->pages_per_split = (int)seg_pages;
 
   struct Chunk { int unit, lo, hi; };
   std::vector<Chunk> wave_chunks;
@@ -173,23 +172,50 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   seg_of_chunk.reserve(wave_units.size() + segs_target + 1);
   std::vector<int> n_chunks_wave(wave_units.size(), 0);
   {
-    int64_t fill = 0;
-    int seg = 0;
-    for (size_t u = 0; u < wave_units.size(); ++u) {
-      int lo = wave_units[u].lo;
-      while (lo < wave_units[u].hi) {
-        const int take = (int)std::min<int64_t>(wave_units[u].hi - lo, seg_pages - fill);
-        wave_chunks.push_back(Chunk{(int)u, lo, lo + take});
-        seg_of_chunk.push_back(seg);
-        n_chunks_wave[u]++;
-        lo += take;
-        fill += take;
-        if (fill == seg_pages) {
-          fill = 0;
-          ++seg;
+    // A chunk's start costs a wave about kChunkStartPages pages of streaming (its item, the query
+    // fragments and the first page ids are dependent reads), so a segment's budget counts each chunk
+    // as its pages plus that start: segments that span several units hold fewer pages.  The budget is
+    // the smallest at which the cut still fits segs_target segments (one round of waves).
+    constexpr int64_t K = kChunkStartPages;
+    auto cut = [&](int64_t cap, bool emit) -> int64_t {  // returns the segment count
+      int64_t fill = 0;
+      int seg = 0;
+      for (size_t u = 0; u < wave_units.size(); ++u) {
+        int lo = wave_units[u].lo;
+        while (lo < wave_units[u].hi) {
+          if (fill > 0 && fill + K >= cap) {  // no room for another start and a page
+            fill = 0;
+            ++seg;
+          }
+          fill += K;
+          const int take = (int)std::min<int64_t>(wave_units[u].hi - lo, cap - fill);
+          if (emit) {
+            wave_chunks.push_back(Chunk{(int)u, lo, lo + take});
+            seg_of_chunk.push_back(seg);
+            n_chunks_wave[u]++;
+          }
+          lo += take;
+          fill += take;
+          if (fill >= cap) {
+            fill = 0;
+            ++seg;
+          }
         }
       }
+      return fill > 0 ? seg + 1 : seg;
+    };
+    int64_t cap = seg_pages + K;  // a single-chunk segment still holds seg_pages pages
+    if (cut(cap, false) > segs_target) {
+      int64_t lo = cap, hi = 2 * cap;
+      while (cut(hi, false) > segs_target) hi *= 2;
+      while (lo + 1 < hi) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        (cut(mid, false) > segs_target ? lo : hi) = mid;
+      }
+      cap = hi;
     }
+    cut(cap, true);
+    plan->pages_per_split = (int)(cap - K);
   }
   // Wide shared-prefix units (LDS-staged workgroup kernel): fixed chunks of kGroupChunkPages pages.
   std::vector<Chunk> group_chunks;

@@ -4,7 +4,8 @@
 // every property the kernels rely on:
 //   decode:  each (sequence, page) pair is read exactly once for its query columns (a shared page once
 //            for every member of the unit that reads it), token ends match the sequence lengths, every
-//            partial slot of a sequence is written exactly once, segments never exceed the split size;
+//            partial slot of a sequence is written exactly once, segments never exceed the split size
+//            (pages plus a start cost per chunk) and fit one round of waves;
 //   prefill: every (session, KV head, query row) is covered exactly once per key range, the key ranges
 //            of a tile tile [0, its last key] without gaps or overlaps;
 //            a split call, and any call of at most one round, keeps every XCD within its share of the
@@ -90,7 +91,14 @@ static bool check_decode(const DecodeCase& c, const DecodePlan& P) {
     int pages = 0;
     for (int k = P.seg_off[s]; k < P.seg_off[s + 1]; ++k) pages += P.wave_items[k].page_hi - P.wave_items[k].page_lo;
     EXPECT(pages <= P.pages_per_split, "segment of %d pages > %d", pages, P.pages_per_split);
+    // a segment's cost counts every chunk start as kChunkStartPages pages; it stays within the budget
+    const int cost = pages + kvp::kChunkStartPages * (P.seg_off[s + 1] - P.seg_off[s]);
+    EXPECT(cost <= P.pages_per_split + kvp::kChunkStartPages, "segment cost %d > %d", cost,
+           P.pages_per_split + kvp::kChunkStartPages);
   }
+  // one round of waves: every segment is taken by Hkv waves of the kDecodeWaves budget
+  EXPECT((int64_t)(P.seg_off.size() - 1) * c.Hkv <= kvp::kDecodeWaves, "%zu segments x %d KV heads > %d waves",
+         P.seg_off.size() - 1, c.Hkv, kvp::kDecodeWaves);
   for (const auto& it : P.wave_items)
     if (!visit(it, true)) return false;
   for (const auto& it : P.group_items)
@@ -344,6 +352,11 @@ static bool self_test() {
     b = P;
     b.wave_items[0].tok_end += 1;  // wrong token end
     expect_reject(b);
+    if (P.seg_off.size() > 2) {
+      b = P;
+      b.seg_off.erase(b.seg_off.begin() + 1);  // two segments given to one wave
+      expect_reject(b);
+    }
   }
   {
     DecodePlan b = P;

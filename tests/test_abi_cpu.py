@@ -78,20 +78,32 @@ def test_plan_covers_every_page_once(name):
     _coverage(w.decode_len, gid, w.shared_pages if gid is not None else None, w.Hq, w.Hkv)
 
 
-def test_plan_segments_are_balanced():
-    """Wave-path chunks are cut into equal page segments whatever the length skew."""
-    w = W.make_workload("mixed")
-    gp = kp.group_prefix(w.group_id, w.shared_pages)
+def _plan_constant(name):
+    import re
+    hdr = open(os.path.join(ROOT, "paper_2608_11152_amd", "csrc", "kvp_plan.h")).read()
+    return int(re.search(rf"constexpr int {name} = (\d+);", hdr).group(1))
+
+
+@pytest.mark.parametrize("name", ["mixed", "rlhf", "agentic"])
+def test_plan_segments_are_balanced(name):
+    """Wave-path chunks are cut into segments of equal cost (pages plus a fixed start cost per chunk)
+    whatever the length skew.  Packed in order into budgets of pages_per_split + that cost (in-order
+    greedy packing uses the fewest budgets), the chunks fill one round of waves, and no chunk is larger
+    than pages_per_split."""
+    w = W.make_workload(name)
+    gp = kp.group_prefix(w.group_id, w.shared_pages) if w.num_groups else None
     items, parts, seg = kp.kvp_plan_decode(w.decode_len, w.Hq, w.Hkv, gp)
     wave = items[(items[:, 0] == 0) | (items[:, 6] * (w.Hq // w.Hkv) <= 16)]
-    pages = int((wave[:, 3] - wave[:, 2]).sum())
-    n_full = pages // seg
-    assert n_full >= 1 and parts < len(items) + w.B
-    # walking the chunks in order, the running page count crosses every multiple of seg exactly at a
-    # chunk boundary (segments are exactly seg pages, except the last)
-    run = np.cumsum(wave[:, 3] - wave[:, 2])
-    for k in range(1, n_full + 1):
-        assert k * seg in set(run.tolist())
+    K, waves = _plan_constant("kChunkStartPages"), _plan_constant("kDecodeWaves")
+    pages = (wave[:, 3] - wave[:, 2]).tolist()
+    # a shared-prefix chunk gives each of its members a partial; a sequence splits only at segment ends
+    assert max(pages) <= seg and parts < int(items[:, 6].sum()) + w.B
+    cap, fill, n_seg = seg + K, 0, 1
+    for p in pages:
+        if fill > 0 and fill + K + p > cap:
+            n_seg, fill = n_seg + 1, 0
+        fill += K + p
+    assert n_seg * w.Hkv <= waves, (n_seg, w.Hkv, waves)
 
 
 def test_plan_prefix_counted_once_per_group():
