@@ -352,8 +352,9 @@ int kvp_prefix_table_error(kvp_prefix_table_t table, int* code);
 int kvp_check_tables(const int32_t* block_tables_host, int maxp, const int32_t* lens, int num_seqs,
                      int num_pages, const kvp_group_prefix* gp);
 
-/* Decode work plan, for inspection and tests (pure host computation, no device needed).
- * Writes up to cap items of 8 int32 each into items_out:
+/* Decode work plan, for inspection and tests (pure host computation, no device needed): the plan
+ * paged_decode_attn uses for a bf16 pool (an FP8 pool's segments charge each chunk start more pages,
+ * so their cut can differ).  Writes up to cap items of 8 int32 each into items_out:
  *   {kind (0 = private, 1 = shared prefix), table row, page_lo, page_hi, token_end, first member,
  *    member count, partial slot (-1 = writes the final output)}
  * and returns the item count in *n_items (which may exceed cap), the number of partial slots in

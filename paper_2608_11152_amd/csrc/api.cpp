@@ -342,7 +342,8 @@ struct DecodeLayout {
 
 int layout_decode(kvp_pool_t pool, const int32_t* seq_lens, int B, int maxp, const kvp_group_prefix* gp, int Hq,
                   DecodeLayout* L) {
-  kvp::Status st = kvp::plan_decode(seq_lens, B, maxp, gp, Hq, pool->num_kv_heads, &L->plan);
+  kvp::Status st = kvp::plan_decode(seq_lens, B, maxp, gp, Hq, pool->num_kv_heads, &L->plan,
+                                    pool->dtype == KVP_FP8_E4M3 ? kvp::kChunkStartPagesFp8 : kvp::kChunkStartPages);
   if (!st.ok()) return from_status(st);
   const auto& P = L->plan;
   // One 16-byte record per merged sequence, so a merge workgroup starts from a single read.

@@ -13,7 +13,10 @@ constexpr int kPage = 16;
 constexpr int kMaxColsPerWave = 16;   // query columns one wave's MFMA tile holds (members x heads)
 constexpr int kMaxColsPerGroup = 64;  // query columns one shared-prefix workgroup holds (4 waves)
 constexpr int kMinSegmentPages = 8;   // smallest page count of a decode wave segment
-constexpr int kChunkStartPages = 3;   // a wave chunk's start (item, query and first page ids), in pages
+// A wave chunk's start (its item, query fragments and first page ids are dependent reads) in pages of
+// streaming: bf16 pages, and FP8 pages (half the bytes, so a start is worth more of them).
+constexpr int kChunkStartPages = 3;
+constexpr int kChunkStartPagesFp8 = 5;
 constexpr int kGroupChunkPages = 16;  // pages per workgroup of the LDS-staged shared-prefix kernel
 // Decode waves per call: one round of the waves resident at once on 256 CUs (4 SIMDs x 2 waves each).
 // Sweeps of 1024-16384 put the optimum here on the target workloads.
@@ -77,8 +80,10 @@ struct Status {
 };
 
 Status validate_group_prefix(const int32_t* lens, int B, const kvp_group_prefix* gp);
+// chunk_start_pages: the start cost a segment's budget charges per chunk (kChunkStartPages for bf16
+// pools, kChunkStartPagesFp8 for FP8 pools).
 Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_prefix* gp, int Hq, int Hkv,
-                   DecodePlan* plan);
+                   DecodePlan* plan, int chunk_start_pages = kChunkStartPages);
 Status plan_prefill(const int32_t* ctx_lens, const int32_t* cu_q, int B, int maxp, int Hq, int Hkv,
                     PrefillPlan* plan);
 Status check_tables(const int32_t* bt, int maxp, const int32_t* lens, int B, int num_pages,

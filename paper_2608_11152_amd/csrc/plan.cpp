@@ -1,6 +1,6 @@
 // Host planner: validates host metadata and builds the work lists of the decode and prefill kernels.
-// Deterministic: a plan depends only on lengths, group structure and head counts, never on physical
-// page ids, so GPU results are bitwise reproducible under any page permutation.
+// Deterministic: a plan depends only on lengths, group structure, head counts and the pool's element
+// type, never on physical page ids, so GPU results are bitwise reproducible under any page permutation.
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
@@ -45,13 +45,14 @@ Status validate_group_prefix(const int32_t* lens, int B, const kvp_group_prefix*
 }
 
 Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_prefix* gp, int Hq, int Hkv,
-                   DecodePlan* plan) {
+                   DecodePlan* plan, int chunk_start_pages) {
   *plan = DecodePlan();
   if (B < 0) return fail(KVP_EINVAL, "num_seqs %ld < 0", B);
   if (B > 0 && !seq_lens) return fail(KVP_EINVAL, "seq_lens is NULL");
   if (!supported_gqa(Hq, Hkv))
     return fail(KVP_EUNSUPPORTED, "num_q_heads %ld / num_kv_heads %ld: ratio must be 1, 2, 4, 8 or 16", Hq, Hkv);
   if (maxp < 0) return fail(KVP_EINVAL, "maxp %ld < 0", maxp);
+  if (chunk_start_pages < 0) return fail(KVP_EINVAL, "chunk_start_pages %ld < 0", chunk_start_pages);
   for (int i = 0; i < B; ++i) {
     if (seq_lens[i] < 0) return fail(KVP_EINVAL, "seq_lens[%ld] = %ld < 0", i, seq_lens[i]);
     if ((int64_t)seq_lens[i] > (int64_t)maxp * kPage)
@@ -172,11 +173,11 @@ Status plan_decode(const int32_t* seq_lens, int B, int maxp, const kvp_group_pre
   seg_of_chunk.reserve(wave_units.size() + segs_target + 1);
   std::vector<int> n_chunks_wave(wave_units.size(), 0);
   {
-    // A chunk's start costs a wave about kChunkStartPages pages of streaming (its item, the query
+    // A chunk's start costs a wave about chunk_start_pages pages of streaming (its item, the query
     // fragments and the first page ids are dependent reads), so a segment's budget counts each chunk
     // as its pages plus that start: segments that span several units hold fewer pages.  The budget is
     // the smallest at which the cut still fits segs_target segments (one round of waves).
-    constexpr int64_t K = kChunkStartPages;
+    const int64_t K = chunk_start_pages;
     auto cut = [&](int64_t cap, bool emit) -> int64_t {  // returns the segment count
       int64_t fill = 0;
       int seg = 0;

@@ -43,7 +43,7 @@ struct DecodeCase {
   int Hq = 32, Hkv = 4, maxp = 0;
 };
 
-static bool check_decode(const DecodeCase& c, const DecodePlan& P) {
+static bool check_decode(const DecodeCase& c, const DecodePlan& P, int K = kvp::kChunkStartPages) {
   const int B = (int)c.lens.size();
   std::vector<std::vector<int>> seen(B);
   for (int i = 0; i < B; ++i) seen[i].assign((c.lens[i] + 15) / 16, 0);
@@ -91,10 +91,9 @@ static bool check_decode(const DecodeCase& c, const DecodePlan& P) {
     int pages = 0;
     for (int k = P.seg_off[s]; k < P.seg_off[s + 1]; ++k) pages += P.wave_items[k].page_hi - P.wave_items[k].page_lo;
     EXPECT(pages <= P.pages_per_split, "segment of %d pages > %d", pages, P.pages_per_split);
-    // a segment's cost counts every chunk start as kChunkStartPages pages; it stays within the budget
-    const int cost = pages + kvp::kChunkStartPages * (P.seg_off[s + 1] - P.seg_off[s]);
-    EXPECT(cost <= P.pages_per_split + kvp::kChunkStartPages, "segment cost %d > %d", cost,
-           P.pages_per_split + kvp::kChunkStartPages);
+    // a segment's cost counts every chunk start as K pages; it stays within the budget
+    const int cost = pages + K * (P.seg_off[s + 1] - P.seg_off[s]);
+    EXPECT(cost <= P.pages_per_split + K, "segment cost %d > %d", cost, P.pages_per_split + K);
   }
   // one round of waves: every segment is taken by Hkv waves of the kDecodeWaves budget
   EXPECT((int64_t)(P.seg_off.size() - 1) * c.Hkv <= kvp::kDecodeWaves, "%zu segments x %d KV heads > %d waves",
@@ -265,7 +264,12 @@ static bool run_decode(const DecodeCase& c) {
   EXPECT(s.ok(), "plan_decode failed: %s", s.msg.c_str());
   kvp::plan_decode(c.lens.data(), (int)c.lens.size(), c.maxp, &gp, c.Hq, c.Hkv, &Q);
   EXPECT(same_plan(P, Q), "plan_decode is not deterministic");
-  return check_decode(c, P);
+  if (!check_decode(c, P)) return false;
+  // the FP8-pool plan: the same properties under its larger chunk-start cost
+  DecodePlan F;
+  s = kvp::plan_decode(c.lens.data(), (int)c.lens.size(), c.maxp, &gp, c.Hq, c.Hkv, &F, kvp::kChunkStartPagesFp8);
+  EXPECT(s.ok(), "plan_decode (FP8 cost) failed: %s", s.msg.c_str());
+  return check_decode(c, F, kvp::kChunkStartPagesFp8);
 }
 
 static int g_split_sessions = 0;
